@@ -1,0 +1,10 @@
+"""CPU oracle for the linear-layer online prefill (test infrastructure only).
+
+Only the test-suite, the smoke check and the benchmark's CPU-baseline leg may
+import this package.  It shares no code with the GPU library.
+"""
+from .core import (gdn_scan, gdn_transition, ssd_scan, ssd_log_decay, init_single,
+                   compose_gdn, compose_ssd, load)
+
+__all__ = ["gdn_scan", "gdn_transition", "ssd_scan", "ssd_log_decay", "init_single",
+           "compose_gdn", "compose_ssd", "load"]
