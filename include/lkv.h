@@ -1,0 +1,172 @@
+/*
+ * lkv.h -- C ABI of liblkv.so, the gfx950 (MI355X) implementation of one
+ * recurrent layer's online prefill in LinearKV's hybrid position-independent
+ * caching: initialise the layer's state from K cached per-block states, then
+ * run the chunkwise recurrence over the request's online tokens.
+ *
+ * Notation.  For one value head the state is S in R^{dv x dk}, row-major
+ * (dk contiguous).  The paper writes the state as its transpose, S_paper in
+ * R^{dk x dv} with S_i = T_i S_{i-1} + u_i (Sec. 2, Eq. 1); here the same
+ * recurrence is S_t = S_{t-1} A_t + (update), with
+ *   Gated DeltaNet (Eq. 3): A_t = alpha_t (I - beta_t k_t k_t^T),
+ *       alpha_t = exp(g_t), update beta_t v_t k_t^T, output o_t = scale * S_t q_t;
+ *   Mamba-2 (Eq. 2): A_t = exp(dt_t A_h) I, update dt_t x_t B_t^T,
+ *       output y_t = S_t C_t.
+ * A block of tokens maps any incoming state to S_out = S_in M + B (Eq. 5):
+ * B is the state it reaches from zero, M = A_1 ... A_L its transition (a dense
+ * dk x dk matrix for Gated DeltaNet, the scalar exp(Lambda), Lambda =
+ * A_h sum dt, for Mamba-2).
+ *
+ * Memory.  Every pointer argument that names tensor data is a DEVICE pointer
+ * owned by the caller; the library never allocates, frees or synchronises.
+ * Tensors are dense, row-major, and 16-byte aligned.  Token streams are packed
+ * "THD": [n_tok, heads, dim] over consecutive segments, cu[s]..cu[s+1] being
+ * segment s's tokens.  Value head h reads q/k head h / (h_v / h_qk).
+ *
+ * Calls.  Every call validates its arguments on the host, enqueues its kernels
+ * on `stream` (a hipStream_t; NULL = the null stream) and returns without
+ * waiting.  Outputs are fully overwritten.  Results are deterministic: the
+ * same inputs give bitwise-identical outputs run to run.  Argument errors are
+ * reported synchronously through the return code; a failed launch returns
+ * LKV_E_HIP and lkv_last_hip_error() gives the HIP code.  Device-side index
+ * checks never fault: segment offsets are clamped to [0, n_tok], and a block
+ * index outside [0, n_blk) turns that request's whole output slice into NaN.
+ * Calls that overlap on one stream are ordered by the stream; calls on
+ * different streams that share an output race.
+ */
+#ifndef LKV_H
+#define LKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LKV_ABI_VERSION 1
+
+typedef enum {
+    LKV_OK = 0,
+    LKV_E_NULL = 1,         /* a required pointer is NULL                         */
+    LKV_E_SHAPE = 2,        /* a size is negative, zero where it may not be, or inconsistent */
+    LKV_E_DTYPE = 3,        /* unknown or unsupported dtype for this argument        */
+    LKV_E_ALIGN = 4,        /* a tensor pointer is not 16-byte aligned               */
+    LKV_E_UNSUPPORTED = 5,  /* a valid geometry this build does not implement        */
+    LKV_E_HIP = 7           /* the HIP runtime reported an error (lkv_last_hip_error) */
+} lkv_status;
+
+typedef enum { LKV_F32 = 0, LKV_BF16 = 1 } lkv_dtype;
+typedef enum { LKV_GDN = 0, LKV_SSD = 1 } lkv_family;
+
+/* Geometry of one recurrent layer.
+ *   family     LKV_GDN | LKV_SSD
+ *   h_qk       GDN: q/k heads        | SSD: B/C groups G           (h_v % h_qk == 0)
+ *   h_v        GDN: value heads      | SSD: heads H                (one state each)
+ *   dk         GDN: key dim          | SSD: state dim N            in {16, 32, 64, 128}
+ *   dv         GDN: value dim        | SSD: head dim P             multiple of 16, <= 512
+ *   chunk      tokens per chunk of the chunkwise kernels           in {16, 64}
+ *   io_dtype   dtype of q/k/v (C/B/x) and o (y)                    LKV_F32 | LKV_BF16
+ *   gate_dtype GDN: dtype of g = log(alpha) and beta               LKV_F32 | LKV_BF16
+ *              SSD: must be LKV_F32 (dt)                                              */
+typedef struct {
+    int32_t family;
+    int32_t h_qk;
+    int32_t h_v;
+    int32_t dk;
+    int32_t dv;
+    int32_t chunk;
+    int32_t io_dtype;
+    int32_t gate_dtype;
+} lkv_layer;
+
+/* One packed token stream over n_seq segments (cached blocks or requests).
+ *   cu       device int32 [n_seq+1], cu[0] = 0, non-decreasing, cu[n_seq] = n_tok
+ *   n_seq    number of segments (>= 0)
+ *   n_tok    host copy of cu[n_seq]
+ *   q        GDN q [n_tok,h_qk,dk] | SSD C [n_tok,G,N]   (unused by lkv_block_summary)
+ *   k        GDN k [n_tok,h_qk,dk] | SSD B [n_tok,G,N]
+ *   v        GDN v [n_tok,h_v,dv]  | SSD x [n_tok,H,P]
+ *   g        GDN g = log(alpha) [n_tok,h_v] (gate_dtype) | SSD dt [n_tok,H] f32, > 0
+ *   beta     GDN beta [n_tok,h_v] (gate_dtype)           | SSD unused (NULL)
+ *   A        GDN unused (NULL)                           | SSD A [H] f32, < 0          */
+typedef struct {
+    const int32_t* cu;
+    int32_t n_seq;
+    int64_t n_tok;
+    const void* q;
+    const void* k;
+    const void* v;
+    const void* g;
+    const void* beta;
+    const float* A;
+} lkv_tokens;
+
+/* ABI version of the loaded library (LKV_ABI_VERSION). */
+int lkv_abi_version(void);
+
+/* Static English text for a status code. */
+const char* lkv_status_string(lkv_status s);
+
+/* hipError_t behind the last LKV_E_HIP returned on the calling thread. */
+int lkv_last_hip_error(void);
+
+/* Per-block summary (Eq. 5): for every segment of `blocks`, scanned from an
+ * empty start, write
+ *   B_out  [n_blk,h_v,dv,dk] f32   the block's final state from zero (S_local)
+ *   M_out  GDN: [n_blk,h_v,dk,dk] f32, M = A_1...A_L, row-major M[i][j]
+ *          SSD: [n_blk,H] f32, the log-decay Lambda = A_h * sum_t dt_t
+ * Either output may be NULL (then it is not computed); not both.
+ * blocks->q is not read.  Errors: LKV_E_NULL, LKV_E_SHAPE, LKV_E_DTYPE,
+ * LKV_E_ALIGN, LKV_E_UNSUPPORTED, LKV_E_HIP. */
+lkv_status lkv_block_summary(const lkv_layer* layer, const lkv_tokens* blocks,
+                             float* B_out, float* M_out, void* stream);
+
+/* Single-block initialisation (Sec. 3.2, "single-block initialization"):
+ *   S_init[r] = B_pool[src_blk[r]]   (bit-exact copy), for r < n_req.
+ *   B_pool   [n_blk,h_v,dv,dk] f32 device
+ *   src_blk  device int32 [n_req]; -1 gives a zero state; any other value
+ *            outside [0, n_blk) gives a NaN slice
+ *   S_init   [n_req,h_v,dv,dk] f32 device; must not overlap B_pool
+ * The paper's default picks each request's last matched block; any choice
+ * (e.g. a random block, its App. A variant) is the caller's. */
+lkv_status lkv_init_single(const lkv_layer* layer, int32_t n_req, int32_t n_blk,
+                           const float* B_pool, const int32_t* src_blk, float* S_init,
+                           void* stream);
+
+/* Exact composition (Eq. 6, evaluated as Eq. 5 applied block after block from
+ * an empty prefix): for request r with blocks b_1..b_K (context order)
+ *   S <- B_{b_1};  S <- S M_{b_j} + B_{b_j} for j = 2..K;  S_init[r] = S
+ * (Mamba-2: S <- exp(Lambda_{b_j}) S + B_{b_j}).  K = 0 gives zeros.
+ *   B_pool   [n_blk,h_v,dv,dk] f32 device
+ *   M_pool   GDN [n_blk,h_v,dk,dk] f32 (row-major M) | SSD [n_blk,H] f32 Lambda.
+ *            The entry of each request's first block is never read.
+ *   blk_ids  device int32 [n_ids]: every request's pool rows, concatenated
+ *   blk_cu   device int32 [n_req+1]: request r uses blk_ids[blk_cu[r]..blk_cu[r+1]),
+ *            clamped to [0, n_ids]; an id outside [0, n_blk) gives a NaN slice
+ *   n_ids    host copy of blk_cu[n_req]
+ *   S_init   [n_req,h_v,dv,dk] f32 device; must not overlap the pools          */
+lkv_status lkv_init_compose(const lkv_layer* layer, int32_t n_req, int32_t n_blk,
+                            const float* B_pool, const float* M_pool,
+                            const int32_t* blk_ids, const int32_t* blk_cu, int32_t n_ids,
+                            float* S_init, void* stream);
+
+/* Gated DeltaNet chunkwise scan over each request's online tokens (Alg. 1,
+ * recompute step; Eq. 1 and Eq. 3), starting from S_init:
+ *   o[t]     = scale * S_t q_t, stored in io_dtype, [n_tok,h_v,dv]
+ *   S_final  [n_req,h_v,dv,dk] f32, the state after the last token
+ * S_init may be NULL (zero start) and may equal S_final (in place).
+ * o may be NULL (state only).  layer->family must be LKV_GDN. */
+lkv_status lkv_gdn_chunk_scan(const lkv_layer* layer, const lkv_tokens* online, float scale,
+                              const float* S_init, void* o, float* S_final, void* stream);
+
+/* Mamba-2 (SSD) chunkwise scan (Eq. 1 and Eq. 2): y[t] = S_t C_t in io_dtype
+ * [n_tok,H,P]; S_final [n_req,H,P,N] f32.  S_init may be NULL or equal
+ * S_final; y may be NULL.  layer->family must be LKV_SSD. */
+lkv_status lkv_ssd_chunk_scan(const lkv_layer* layer, const lkv_tokens* online,
+                              const float* S_init, void* y, float* S_final, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LKV_H */

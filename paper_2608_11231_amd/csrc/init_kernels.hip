@@ -1,0 +1,223 @@
+// State initialisation kernels: single-block gather (Sec. 3.2) and exact
+// composition of per-block (M, B) pairs (Eq. 5 applied block after block,
+// which telescopes to Eq. 6).
+#include "init_kernels.h"
+
+#include <math.h>
+
+namespace lkv {
+
+// ---------------------------------------------------------------- single block
+// S_init[r] = B_pool[src[r]]: a bit-exact 16-byte-vector copy, HBM-bound.
+// One thread per float4 of the output; request r = index / per_req.
+__global__ __launch_bounds__(256) void init_single_kernel(int32_t n_req, int32_t n_blk, int64_t per_req4,
+                                                          const f32x4* __restrict__ B_pool,
+                                                          const int32_t* __restrict__ src,
+                                                          f32x4* __restrict__ S) {
+    const int64_t total = (int64_t)n_req * per_req4;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
+        const int64_t r = i / per_req4, e = i - r * per_req4;
+        const int32_t id = src[r];
+        f32x4 v;
+        if (id >= 0 && id < n_blk) {
+            v = __builtin_nontemporal_load(B_pool + (int64_t)id * per_req4 + e);
+        } else {
+            const float f = (id == -1) ? 0.f : __builtin_nanf("");
+            v = f32x4{f, f, f, f};
+        }
+        __builtin_nontemporal_store(v, S + i);
+    }
+}
+
+hipError_t launch_init_single(int32_t n_req, int32_t n_blk, int64_t per_req, const float* B_pool,
+                              const int32_t* src, float* S, hipStream_t st) {
+    const int64_t per4 = per_req / 4;
+    const int64_t total = (int64_t)n_req * per4;
+    if (total == 0) return hipSuccess;
+    int64_t blocks = (total + 255) / 256;
+    if (blocks > 256 * 16) blocks = 256 * 16;
+    hipLaunchKernelGGL(init_single_kernel, dim3((unsigned)blocks), dim3(256), 0, st, n_req, n_blk, per4,
+                       reinterpret_cast<const f32x4*>(B_pool), src, reinterpret_cast<f32x4*>(S));
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- Mamba-2 composition
+// S <- B_{b_1}; S <- exp(Lambda_{b_j}) S + B_{b_j}.  Elementwise over the state.
+__global__ __launch_bounds__(256) void compose_ssd_kernel(int32_t n_req, int32_t n_blk, int32_t H,
+                                                          int64_t per_head4, const f32x4* __restrict__ B_pool,
+                                                          const float* __restrict__ Lam,
+                                                          const int32_t* __restrict__ ids,
+                                                          const int32_t* __restrict__ blk_cu, int32_t n_ids,
+                                                          f32x4* __restrict__ S) {
+    const int64_t total = (int64_t)n_req * H * per_head4;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
+        const int64_t rh = i / per_head4, e = i - rh * per_head4;
+        const int32_t r = (int32_t)(rh / H), h = (int32_t)(rh - (int64_t)r * H);
+        int32_t b0 = blk_cu[r], b1 = blk_cu[r + 1];
+        b0 = b0 < 0 ? 0 : (b0 > n_ids ? n_ids : b0);
+        b1 = b1 < b0 ? b0 : (b1 > n_ids ? n_ids : b1);
+        f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+        bool bad = false;
+        for (int32_t j = b0; j < b1; ++j) {
+            const int32_t id = ids[j];
+            if (id < 0 || id >= n_blk) { bad = true; break; }
+            const f32x4 b = B_pool[((int64_t)id * H + h) * per_head4 + e];
+            if (j == b0) {
+                acc = b;
+            } else {
+                const float a = __expf(Lam[(int64_t)id * H + h]);
+                acc = a * acc + b;
+            }
+        }
+        if (bad) {
+            const float f = __builtin_nanf("");
+            acc = f32x4{f, f, f, f};
+        }
+        S[i] = acc;
+    }
+}
+
+hipError_t launch_compose_ssd(int32_t n_req, int32_t n_blk, int32_t H, int64_t per_head, const float* B_pool,
+                              const float* Lam, const int32_t* ids, const int32_t* blk_cu, int32_t n_ids,
+                              float* S, hipStream_t st) {
+    const int64_t total = (int64_t)n_req * H * (per_head / 4);
+    if (total == 0) return hipSuccess;
+    int64_t blocks = (total + 255) / 256;
+    if (blocks > 256 * 16) blocks = 256 * 16;
+    hipLaunchKernelGGL(compose_ssd_kernel, dim3((unsigned)blocks), dim3(256), 0, st, n_req, n_blk, H,
+                       per_head / 4, reinterpret_cast<const f32x4*>(B_pool), Lam, ids, blk_cu, n_ids,
+                       reinterpret_cast<f32x4*>(S));
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- Gated DeltaNet composition
+// Work unit = (request, head, tile of 16*nw state rows); wave w owns rows
+// row0 + 16w + (lane % 16).  The state stays in registers in acc-tile layout
+// (tile nt: S[row][16nt + 4g + r]), which is directly the B operand of
+//   S_new^T = M^T S^T    (contraction over the state's dk index),
+// so each step needs only M^T staged in LDS, split into bf16 hi/lo planes
+// (products Mh*Sh + Mh*Sl + Ml*Sh keep the fp32 chain at ~1e-5 relative).
+template <int DK>
+struct ComposeLds {
+    static constexpr int SM = DK + 8;
+    static __host__ __device__ constexpr size_t bytes() { return size_t(2) * DK * SM * 2; }
+};
+
+template <int DK>
+__global__ __launch_bounds__(256) void compose_gdn_kernel(ComposeArgs p) {
+    constexpr int NTK = DK / 16, SM = ComposeLds<DK>::SM;
+    extern __shared__ __align__(16) char smem[];
+    bf16* sMh = reinterpret_cast<bf16*>(smem);
+    bf16* sMl = sMh + DK * SM;
+    const int nw = p.nw, nthreads = 64 * nw, tid = threadIdx.x;
+    const int w = tid >> 6, lane = tid & 63, g = lane >> 4, c16 = lane & 15;
+    const int u = xcd_unit(blockIdx.x, p.n_units);
+    const int tile = u % p.tiles;
+    const int h = (u / p.tiles) % p.h_v;
+    const int r = u / (p.tiles * p.h_v);
+    const int my_row = tile * 16 * nw + 16 * w + c16;
+
+    int32_t b0 = p.blk_cu[r], b1 = p.blk_cu[r + 1];
+    b0 = b0 < 0 ? 0 : (b0 > p.n_ids ? p.n_ids : b0);
+    b1 = b1 < b0 ? b0 : (b1 > p.n_ids ? p.n_ids : b1);
+
+    f32x4 S[NTK];
+#pragma unroll
+    for (int nt = 0; nt < NTK; ++nt) S[nt] = zero4();
+    bool bad = false;
+    for (int32_t j = b0; j < b1; ++j) {
+        const int32_t id = p.blk_ids[j];
+        if (id < 0 || id >= p.n_blk) { bad = true; break; }
+        const float* Bj = p.B_pool + (((int64_t)id * p.h_v + h) * p.dv + my_row) * DK + 4 * g;
+        if (j == b0) {
+#pragma unroll
+            for (int nt = 0; nt < NTK; ++nt) S[nt] = *reinterpret_cast<const f32x4*>(Bj + 16 * nt);
+            continue;
+        }
+        // stage M^T (split) : sM[jj][ii] = M[ii][jj]
+        const float* Mj = p.M_pool + ((int64_t)id * p.h_v + h) * DK * DK;
+        __syncthreads();
+        for (int idx = tid; idx < DK * DK / 4; idx += nthreads) {
+            const int ii = idx / (DK / 4), jj = (idx % (DK / 4)) * 4;
+            const Split4 sp = split4(*reinterpret_cast<const f32x4*>(Mj + ii * DK + jj));
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                sMh[(jj + e) * SM + ii] = sp.hi[e];
+                sMl[(jj + e) * SM + ii] = sp.lo[e];
+            }
+        }
+        __syncthreads();
+        bf16x4 Sh[NTK], Sl[NTK];
+#pragma unroll
+        for (int nt = 0; nt < NTK; ++nt) {
+            const Split4 sp = split4(S[nt]);
+            Sh[nt] = sp.hi;
+            Sl[nt] = sp.lo;
+        }
+#pragma unroll
+        for (int nt = 0; nt < NTK; ++nt) {
+            const bf16* mh = sMh + (16 * nt + c16) * SM;
+            const bf16* ml = sMl + (16 * nt + c16) * SM;
+            f32x4 acc = *reinterpret_cast<const f32x4*>(Bj + 16 * nt);
+            int kg = 0;
+#pragma unroll
+            for (; kg + 1 < NTK; kg += 2) {
+                const bf16x4 a0 = lds4(mh + 16 * kg + 4 * g), a1 = lds4(mh + 16 * kg + 16 + 4 * g);
+                const bf16x4 c0 = lds4(ml + 16 * kg + 4 * g), c1 = lds4(ml + 16 * kg + 16 + 4 * g);
+                acc = mma32(a0, a1, Sh[kg], Sh[kg + 1], acc);
+                acc = mma32(a0, a1, Sl[kg], Sl[kg + 1], acc);
+                acc = mma32(c0, c1, Sh[kg], Sh[kg + 1], acc);
+            }
+            if (NTK & 1) {
+                const bf16x4 a0 = lds4(mh + 16 * kg + 4 * g), c0 = lds4(ml + 16 * kg + 4 * g);
+                acc = mma16(a0, Sh[kg], acc);
+                acc = mma16(a0, Sl[kg], acc);
+                acc = mma16(c0, Sh[kg], acc);
+            }
+            S[nt] = acc;
+        }
+    }
+    if (bad) {
+        const float f = __builtin_nanf("");
+#pragma unroll
+        for (int nt = 0; nt < NTK; ++nt) S[nt] = f32x4{f, f, f, f};
+    }
+    float* dst = p.S + (((int64_t)r * p.h_v + h) * p.dv + my_row) * DK + 4 * g;
+#pragma unroll
+    for (int nt = 0; nt < NTK; ++nt) *reinterpret_cast<f32x4*>(dst + 16 * nt) = S[nt];
+}
+
+size_t compose_gdn_lds_bytes(int dk) {
+    switch (dk) {
+        case 16: return ComposeLds<16>::bytes();
+        case 32: return ComposeLds<32>::bytes();
+        case 64: return ComposeLds<64>::bytes();
+        case 128: return ComposeLds<128>::bytes();
+    }
+    return 0;
+}
+
+template <int DK>
+static hipError_t launch_compose_gdn_t(const ComposeArgs& a, hipStream_t st) {
+    const size_t lds = ComposeLds<DK>::bytes();
+    auto kern = compose_gdn_kernel<DK>;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kern, dim3(a.n_units), dim3(64 * a.nw), lds, st, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_compose_gdn(int dk, const ComposeArgs& a, hipStream_t st) {
+    switch (dk) {
+        case 16: return launch_compose_gdn_t<16>(a, st);
+        case 32: return launch_compose_gdn_t<32>(a, st);
+        case 64: return launch_compose_gdn_t<64>(a, st);
+        case 128: return launch_compose_gdn_t<128>(a, st);
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace lkv

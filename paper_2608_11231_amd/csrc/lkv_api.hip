@@ -1,0 +1,257 @@
+// C ABI of liblkv.so (declared in include/lkv.h): host-side validation,
+// launch-geometry selection and dispatch to the gfx950 kernels.
+#include <stdlib.h>
+
+#include "init_kernels.h"
+#include "lkv.h"
+#include "scan_kernel.h"
+
+using namespace lkv;
+
+namespace {
+
+thread_local int g_last_hip = 0;
+
+lkv_status hip_status(hipError_t e) {
+    if (e == hipSuccess) return LKV_OK;
+    g_last_hip = (int)e;
+    return LKV_E_HIP;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+lkv_status check_layer(const lkv_layer* L) {
+    if (!L) return LKV_E_NULL;
+    if (L->family != LKV_GDN && L->family != LKV_SSD) return LKV_E_SHAPE;
+    if (L->h_qk < 1 || L->h_v < 1 || L->h_v % L->h_qk != 0) return LKV_E_SHAPE;
+    if (L->dk < 1 || L->dv < 1 || L->chunk < 1) return LKV_E_SHAPE;
+    if (L->io_dtype != LKV_F32 && L->io_dtype != LKV_BF16) return LKV_E_DTYPE;
+    if (L->gate_dtype != LKV_F32 && L->gate_dtype != LKV_BF16) return LKV_E_DTYPE;
+    if (L->family == LKV_SSD && L->gate_dtype != LKV_F32) return LKV_E_DTYPE;
+    if (L->dk != 16 && L->dk != 32 && L->dk != 64 && L->dk != 128) return LKV_E_UNSUPPORTED;
+    if (L->dv % 16 != 0 || L->dv > 512) return LKV_E_UNSUPPORTED;
+    if (L->chunk != 16 && L->chunk != 64) return LKV_E_UNSUPPORTED;
+    return LKV_OK;
+}
+
+int env_int(const char* name, int dflt) {
+    const char* s = getenv(name);
+    return s ? atoi(s) : dflt;
+}
+
+// Waves per workgroup for the chunk kernels: 16*nw state rows per workgroup.
+// More waves share the token x token work of a chunk; fewer waves give more
+// workgroups.  Pick the largest nw that still fills the 256 CUs.
+int pick_nw(int fam, int dk, int chunk, bool f32io, int64_t pairs, int rows, int rows2) {
+    int forced = env_int("LKV_SCAN_NW", 0);
+    for (int nw = 4; nw >= 1; nw >>= 1) {
+        if (rows % (16 * nw) || (rows2 && rows2 % (16 * nw))) continue;
+        if (scan_lds_bytes(fam, dk, chunk, f32io, nw) > 160 * 1024) continue;
+        if (forced) {
+            if (nw == forced) return nw;
+            continue;
+        }
+        const int64_t units = pairs * ((rows + (rows2 ? rows2 : 0)) / (16 * nw));
+        if (units >= 240 || nw == 1) return nw;
+    }
+    return 1;
+}
+
+lkv_status check_tokens(const lkv_layer* L, const lkv_tokens* T, bool need_q) {
+    if (!T) return LKV_E_NULL;
+    if (T->n_seq < 0 || T->n_tok < 0) return LKV_E_SHAPE;
+    if (T->n_seq > 0 && !T->cu) return LKV_E_NULL;
+    if (T->n_tok > 0) {
+        if (!T->k || !T->v || !T->g) return LKV_E_NULL;
+        if (need_q && !T->q) return LKV_E_NULL;
+        if (L->family == LKV_GDN && !T->beta) return LKV_E_NULL;
+        if (!aligned16(T->k) || !aligned16(T->v) || (need_q && !aligned16(T->q))) return LKV_E_ALIGN;
+    }
+    if (L->family == LKV_SSD && T->n_seq > 0 && !T->A) return LKV_E_NULL;
+    if (T->n_tok > INT64_C(1) << 40) return LKV_E_SHAPE;
+    return LKV_OK;
+}
+
+ScanArgs base_args(const lkv_layer* L, const lkv_tokens* T) {
+    ScanArgs a = {};
+    a.cu = T->cu;
+    a.n_seq = T->n_seq;
+    a.n_tok = T->n_tok;
+    a.q = T->q;
+    a.k = T->k;
+    a.v = T->v;
+    a.g = T->g;
+    a.beta = T->beta;
+    a.A = T->A;
+    a.h_qk = L->h_qk;
+    a.h_v = L->h_v;
+    a.dv = L->dv;
+    a.gate_bf16 = L->gate_dtype == LKV_BF16;
+    a.scale = 1.f;
+    return a;
+}
+
+hipError_t launch_scan(const lkv_layer* L, const ScanArgs& a, hipStream_t st) {
+    const bool f32io = L->io_dtype == LKV_F32;
+    return L->family == LKV_GDN ? launch_scan_gdn(L->dk, L->chunk, f32io, a, st)
+                                : launch_scan_ssd(L->dk, L->chunk, f32io, a, st);
+}
+
+lkv_status chunk_scan(const lkv_layer* L, const lkv_tokens* T, float scale, const float* S_init, void* out,
+                      float* S_final, void* stream) {
+    lkv_status s = check_tokens(L, T, out != nullptr);
+    if (s != LKV_OK) return s;
+    if ((S_init && !aligned16(S_init)) || (S_final && !aligned16(S_final))) return LKV_E_ALIGN;
+    if (T->n_seq == 0) return LKV_OK;
+    if (!out && !S_final) return LKV_OK;
+    const bool f32io = L->io_dtype == LKV_F32;
+    const int64_t pairs = (int64_t)T->n_seq * L->h_v;
+    const int nw = pick_nw(L->family, L->dk, L->chunk, f32io, pairs, L->dv, 0);
+    const int64_t units = pairs * (L->dv / (16 * nw));
+    if (units >= (INT64_C(1) << 31)) return LKV_E_SHAPE;
+    ScanArgs a = base_args(L, T);
+    a.scale = scale;
+    a.S_init = S_init;
+    a.out = out;
+    a.S_final = S_final;
+    a.summary = 0;
+    a.tiles_b = L->dv / (16 * nw);
+    a.tiles_m = 0;
+    a.nw = nw;
+    a.n_units = (int32_t)units;
+    return hip_status(launch_scan(L, a, (hipStream_t)stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+int lkv_abi_version(void) { return LKV_ABI_VERSION; }
+
+const char* lkv_status_string(lkv_status s) {
+    switch (s) {
+        case LKV_OK: return "ok";
+        case LKV_E_NULL: return "a required pointer is NULL";
+        case LKV_E_SHAPE: return "invalid or inconsistent size";
+        case LKV_E_DTYPE: return "unsupported dtype";
+        case LKV_E_ALIGN: return "tensor pointer not 16-byte aligned";
+        case LKV_E_UNSUPPORTED: return "geometry not implemented by this build";
+        case LKV_E_HIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+int lkv_last_hip_error(void) { return g_last_hip; }
+
+lkv_status lkv_block_summary(const lkv_layer* L, const lkv_tokens* T, float* B_out, float* M_out,
+                             void* stream) {
+    lkv_status s = check_layer(L);
+    if (s != LKV_OK) return s;
+    if (!B_out && !M_out) return LKV_E_NULL;
+    s = check_tokens(L, T, false);
+    if (s != LKV_OK) return s;
+    if ((B_out && !aligned16(B_out)) || (M_out && !aligned16(M_out))) return LKV_E_ALIGN;
+    if (T->n_seq == 0) return LKV_OK;
+    const bool f32io = L->io_dtype == LKV_F32;
+    const int64_t pairs = (int64_t)T->n_seq * L->h_v;
+    const bool gdn_m = L->family == LKV_GDN && M_out;
+    const int rows_b = B_out ? L->dv : 0;
+    const int rows_m = gdn_m ? L->dk : 0;
+    ScanArgs a = base_args(L, T);
+    a.summary = 1;
+    a.S_final = B_out;
+    a.M_out = M_out;
+    hipStream_t st = (hipStream_t)stream;
+    if (L->family == LKV_SSD && !B_out) {
+        // Lambda only: one row tile per (block, head) carries the gate sum
+        a.nw = 1;
+        a.tiles_b = 1;
+        a.tiles_m = 0;
+        a.S_final = nullptr;
+        const int64_t units = pairs;
+        if (units >= (INT64_C(1) << 31)) return LKV_E_SHAPE;
+        a.n_units = (int32_t)units;
+        return hip_status(launch_scan(L, a, st));
+    }
+    const int nw = pick_nw(L->family, L->dk, L->chunk, f32io, pairs, rows_b ? rows_b : rows_m,
+                           rows_b ? rows_m : 0);
+    a.nw = nw;
+    a.tiles_b = rows_b / (16 * nw);
+    a.tiles_m = rows_m / (16 * nw);
+    const int64_t units = pairs * (a.tiles_b + a.tiles_m);
+    if (units >= (INT64_C(1) << 31)) return LKV_E_SHAPE;
+    a.n_units = (int32_t)units;
+    return hip_status(launch_scan(L, a, st));
+}
+
+lkv_status lkv_init_single(const lkv_layer* L, int32_t n_req, int32_t n_blk, const float* B_pool,
+                           const int32_t* src_blk, float* S_init, void* stream) {
+    lkv_status s = check_layer(L);
+    if (s != LKV_OK) return s;
+    if (n_req < 0 || n_blk < 0) return LKV_E_SHAPE;
+    if (n_req == 0) return LKV_OK;
+    if (!src_blk || !S_init || (n_blk > 0 && !B_pool)) return LKV_E_NULL;
+    if (!aligned16(S_init) || (B_pool && !aligned16(B_pool))) return LKV_E_ALIGN;
+    const int64_t per_req = (int64_t)L->h_v * L->dv * L->dk;
+    return hip_status(launch_init_single(n_req, n_blk, per_req, B_pool, src_blk, S_init, (hipStream_t)stream));
+}
+
+lkv_status lkv_init_compose(const lkv_layer* L, int32_t n_req, int32_t n_blk, const float* B_pool,
+                            const float* M_pool, const int32_t* blk_ids, const int32_t* blk_cu, int32_t n_ids,
+                            float* S_init, void* stream) {
+    lkv_status s = check_layer(L);
+    if (s != LKV_OK) return s;
+    if (n_req < 0 || n_blk < 0 || n_ids < 0) return LKV_E_SHAPE;
+    if (n_req == 0) return LKV_OK;
+    if (!blk_cu || !S_init || (n_ids > 0 && !blk_ids)) return LKV_E_NULL;
+    if (n_blk > 0 && (!B_pool || !M_pool)) return LKV_E_NULL;
+    if (!aligned16(S_init) || (B_pool && !aligned16(B_pool)) || (M_pool && !aligned16(M_pool)))
+        return LKV_E_ALIGN;
+    hipStream_t st = (hipStream_t)stream;
+    if (L->family == LKV_SSD) {
+        const int64_t per_head = (int64_t)L->dv * L->dk;
+        return hip_status(launch_compose_ssd(n_req, n_blk, L->h_v, per_head, B_pool, M_pool, blk_ids, blk_cu,
+                                             n_ids, S_init, st));
+    }
+    const int64_t pairs = (int64_t)n_req * L->h_v;
+    int nw = env_int("LKV_COMPOSE_NW", 0);
+    if (nw != 1 && nw != 2 && nw != 4) {
+        nw = 4;
+        while (nw > 1 && (L->dv % (16 * nw) || pairs * (L->dv / (16 * nw)) < 240)) nw >>= 1;
+    }
+    if (L->dv % (16 * nw)) nw = 1;
+    ComposeArgs a = {};
+    a.B_pool = B_pool;
+    a.M_pool = M_pool;
+    a.blk_ids = blk_ids;
+    a.blk_cu = blk_cu;
+    a.n_ids = n_ids;
+    a.n_blk = n_blk;
+    a.h_v = L->h_v;
+    a.dv = L->dv;
+    a.S = S_init;
+    a.nw = nw;
+    a.tiles = L->dv / (16 * nw);
+    const int64_t units = pairs * a.tiles;
+    if (units >= (INT64_C(1) << 31)) return LKV_E_SHAPE;
+    a.n_units = (int32_t)units;
+    return hip_status(launch_compose_gdn(L->dk, a, st));
+}
+
+lkv_status lkv_gdn_chunk_scan(const lkv_layer* L, const lkv_tokens* T, float scale, const float* S_init,
+                              void* o, float* S_final, void* stream) {
+    lkv_status s = check_layer(L);
+    if (s != LKV_OK) return s;
+    if (L->family != LKV_GDN) return LKV_E_SHAPE;
+    return chunk_scan(L, T, scale, S_init, o, S_final, stream);
+}
+
+lkv_status lkv_ssd_chunk_scan(const lkv_layer* L, const lkv_tokens* T, const float* S_init, void* y,
+                              float* S_final, void* stream) {
+    lkv_status s = check_layer(L);
+    if (s != LKV_OK) return s;
+    if (L->family != LKV_SSD) return LKV_E_SHAPE;
+    return chunk_scan(L, T, 1.f, S_init, y, S_final, stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,90 @@
+"""Move seeded workloads (``inputs.Workload``) onto the GPU and run the path.
+
+Marshalling only: tensors are created with torch on the current GPU and the
+computation is done by liblkv.so through ``lkv``.
+"""
+from __future__ import annotations
+
+from typing import Dict, Optional
+
+import numpy as np
+import torch
+
+from . import inputs as I
+from . import lkv
+
+_TORCH = {"bf16": torch.bfloat16, "f32": torch.float32}
+
+
+def layer_struct(layer: I.Layer) -> lkv.Layer:
+    return lkv.make_layer(layer.family, layer.h_qk, layer.h_v, layer.dk, layer.dv, layer.chunk,
+                          _TORCH[layer.io_dtype], _TORCH[layer.gate_dtype])
+
+
+def _t(x: Optional[np.ndarray], dtype, device) -> Optional[torch.Tensor]:
+    if x is None:
+        return None
+    return torch.from_numpy(np.ascontiguousarray(x)).to(device=device, dtype=dtype)
+
+
+class GpuTokens:
+    """A token stream resident in HBM plus its C struct."""
+
+    def __init__(self, tok: I.Tokens, layer: I.Layer, A: Optional[np.ndarray], device="cuda",
+                 with_q: bool = True):
+        io = _TORCH[layer.io_dtype]
+        gate = _TORCH[layer.gate_dtype] if layer.family == I.GDN else torch.float32
+        self.n_tok = tok.n_tok
+        self.cu = _t(tok.cu, torch.int32, device)
+        self.q = _t(tok.q, io, device) if with_q else None
+        self.k = _t(tok.k, io, device)
+        self.v = _t(tok.v, io, device)
+        self.g = _t(tok.g, gate, device)
+        self.beta = _t(tok.beta, gate, device)
+        self.A = _t(A, torch.float32, device) if layer.family == I.SSD else None
+        self.struct = lkv.make_tokens(self.cu, self.n_tok, self.q, self.k, self.v, self.g, self.beta,
+                                      self.A)
+
+
+class GpuWorkload:
+    """All device tensors of a workload: cached blocks, online tokens, index arrays,
+    the block pools and the state buffers."""
+
+    def __init__(self, w: I.Workload, device="cuda", with_cached: bool = True):
+        self.w = w
+        L = w.layer
+        self.layer = layer_struct(L)
+        self.online = GpuTokens(w.online, L, w.A, device)
+        self.cached = GpuTokens(w.cached, L, w.A, device, with_q=False) if with_cached else None
+        self.blk_ids = _t(w.blk_ids, torch.int32, device)
+        self.blk_cu = _t(w.blk_cu, torch.int32, device)
+        self.last_blk = _t(w.last_blk, torch.int32, device)
+        f32 = dict(device=device, dtype=torch.float32)
+        self.B_pool = torch.empty((w.n_blk, L.h_v, L.dv, L.dk), **f32)
+        if L.family == I.GDN:
+            self.M_pool = torch.empty((w.n_blk, L.h_v, L.dk, L.dk), **f32)
+        else:
+            self.M_pool = torch.empty((w.n_blk, L.h_v), **f32)
+        self.S_single = torch.empty((w.n_req, L.h_v, L.dv, L.dk), **f32)
+        self.S_exact = torch.empty_like(self.S_single)
+        self.S_final = torch.empty_like(self.S_single)
+        self.out = torch.empty((w.online.n_tok, L.h_v, L.dv), device=device, dtype=_TORCH[L.io_dtype])
+
+    # -- the path's calls ---------------------------------------------------------
+    def block_summary(self, B: bool = True, M: bool = True, stream=None):
+        lkv.block_summary(self.layer, self.cached.struct, self.B_pool if B else None,
+                          self.M_pool if M else None, stream)
+
+    def init_single(self, stream=None):
+        lkv.init_single(self.layer, self.w.n_blk, self.B_pool, self.last_blk, self.S_single, stream)
+
+    def init_compose(self, stream=None):
+        lkv.init_compose(self.layer, self.w.n_blk, self.B_pool, self.M_pool, self.blk_ids, self.blk_cu,
+                         int(self.w.blk_cu[-1]), self.S_exact, stream)
+
+    def scan(self, S_init: Optional[torch.Tensor], stream=None):
+        if self.w.layer.family == I.GDN:
+            lkv.gdn_chunk_scan(self.layer, self.online.struct, self.w.scale, S_init, self.out, self.S_final,
+                               stream)
+        else:
+            lkv.ssd_chunk_scan(self.layer, self.online.struct, S_init, self.out, self.S_final, stream)

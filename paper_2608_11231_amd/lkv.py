@@ -1,0 +1,155 @@
+"""Thin Python binding of liblkv.so (include/lkv.h).
+
+Argument marshalling only: every function takes torch tensors that already
+live on the GPU, passes their device pointers and the current torch stream to
+the C ABI, and raises ``LkvError`` on a non-zero status.  All computation
+happens in the library's HIP kernels; there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+from typing import Optional
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "liblkv.so")
+
+GDN, SSD = 0, 1
+F32, BF16 = 0, 1
+
+_STATUS = {0: "LKV_OK", 1: "LKV_E_NULL", 2: "LKV_E_SHAPE", 3: "LKV_E_DTYPE", 4: "LKV_E_ALIGN",
+           5: "LKV_E_UNSUPPORTED", 7: "LKV_E_HIP"}
+
+
+class LkvError(RuntimeError):
+    def __init__(self, status: int, call: str, hip: int = 0):
+        self.status = status
+        msg = f"{call}: {_STATUS.get(status, status)}"
+        if status == 7:
+            msg += f" (hipError {hip})"
+        super().__init__(msg)
+
+
+class Layer(ctypes.Structure):
+    _fields_ = [("family", ctypes.c_int32), ("h_qk", ctypes.c_int32), ("h_v", ctypes.c_int32),
+                ("dk", ctypes.c_int32), ("dv", ctypes.c_int32), ("chunk", ctypes.c_int32),
+                ("io_dtype", ctypes.c_int32), ("gate_dtype", ctypes.c_int32)]
+
+
+class Tokens(ctypes.Structure):
+    _fields_ = [("cu", ctypes.c_void_p), ("n_seq", ctypes.c_int32), ("n_tok", ctypes.c_int64),
+                ("q", ctypes.c_void_p), ("k", ctypes.c_void_p), ("v", ctypes.c_void_p),
+                ("g", ctypes.c_void_p), ("beta", ctypes.c_void_p), ("A", ctypes.c_void_p)]
+
+
+_lib = None
+_lock = threading.Lock()
+EXPORTS = ("lkv_abi_version", "lkv_status_string", "lkv_last_hip_error", "lkv_block_summary",
+           "lkv_init_single", "lkv_init_compose", "lkv_gdn_chunk_scan", "lkv_ssd_chunk_scan")
+
+
+def load() -> ctypes.CDLL:
+    """Load liblkv.so; raises if it has not been built."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                                   "`python -m paper_2608_11231_amd.build` (hipcc, gfx950)")
+            lib = ctypes.CDLL(LIB_PATH)
+            vp, i32, f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float
+            LP, TP = ctypes.POINTER(Layer), ctypes.POINTER(Tokens)
+            lib.lkv_abi_version.restype = ctypes.c_int
+            lib.lkv_status_string.restype = ctypes.c_char_p
+            lib.lkv_status_string.argtypes = [ctypes.c_int]
+            lib.lkv_last_hip_error.restype = ctypes.c_int
+            lib.lkv_block_summary.argtypes = [LP, TP, vp, vp, vp]
+            lib.lkv_init_single.argtypes = [LP, i32, i32, vp, vp, vp, vp]
+            lib.lkv_init_compose.argtypes = [LP, i32, i32, vp, vp, vp, vp, i32, vp, vp]
+            lib.lkv_gdn_chunk_scan.argtypes = [LP, TP, f32, vp, vp, vp, vp]
+            lib.lkv_ssd_chunk_scan.argtypes = [LP, TP, vp, vp, vp, vp]
+            for f in ("lkv_block_summary", "lkv_init_single", "lkv_init_compose", "lkv_gdn_chunk_scan",
+                      "lkv_ssd_chunk_scan"):
+                getattr(lib, f).restype = ctypes.c_int
+            _lib = lib
+    return _lib
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if t.device.type != "cuda":
+        raise ValueError("lkv tensors must be on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("lkv tensors must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _check(st: int, call: str):
+    if st != 0:
+        raise LkvError(st, call, load().lkv_last_hip_error())
+
+
+def dtype_code(dt: torch.dtype) -> int:
+    if dt == torch.float32:
+        return F32
+    if dt == torch.bfloat16:
+        return BF16
+    raise ValueError(f"unsupported dtype {dt}")
+
+
+def make_layer(family: int, h_qk: int, h_v: int, dk: int, dv: int, chunk: int,
+               io_dtype: torch.dtype = torch.bfloat16, gate_dtype: torch.dtype = torch.bfloat16) -> Layer:
+    return Layer(family, h_qk, h_v, dk, dv, chunk, dtype_code(io_dtype), dtype_code(gate_dtype))
+
+
+def make_tokens(cu: torch.Tensor, n_tok: int, q=None, k=None, v=None, g=None, beta=None, A=None) -> Tokens:
+    """``cu`` int32 [n_seq+1] on the GPU; ``n_tok`` its last entry (host value)."""
+    t = Tokens()
+    t.cu = _ptr(cu)
+    t.n_seq = int(cu.shape[0]) - 1
+    t.n_tok = int(n_tok)
+    t.q, t.k, t.v, t.g, t.beta, t.A = (_ptr(x) for x in (q, k, v, g, beta, A))
+    t._keep = (cu, q, k, v, g, beta, A)  # keep tensors alive while the struct is in use
+    return t
+
+
+def block_summary(layer: Layer, blocks: Tokens, B_out: Optional[torch.Tensor],
+                  M_out: Optional[torch.Tensor], stream=None) -> None:
+    _check(load().lkv_block_summary(ctypes.byref(layer), ctypes.byref(blocks), _ptr(B_out), _ptr(M_out),
+                                    _stream(stream)), "lkv_block_summary")
+
+
+def init_single(layer: Layer, n_blk: int, B_pool: torch.Tensor, src_blk: torch.Tensor,
+                S_init: torch.Tensor, stream=None) -> None:
+    _check(load().lkv_init_single(ctypes.byref(layer), int(src_blk.shape[0]), int(n_blk), _ptr(B_pool),
+                                  _ptr(src_blk), _ptr(S_init), _stream(stream)), "lkv_init_single")
+
+
+def init_compose(layer: Layer, n_blk: int, B_pool: torch.Tensor, M_pool: torch.Tensor,
+                 blk_ids: torch.Tensor, blk_cu: torch.Tensor, n_ids: int, S_init: torch.Tensor,
+                 stream=None) -> None:
+    _check(load().lkv_init_compose(ctypes.byref(layer), int(blk_cu.shape[0]) - 1, int(n_blk), _ptr(B_pool),
+                                   _ptr(M_pool), _ptr(blk_ids), _ptr(blk_cu), int(n_ids), _ptr(S_init),
+                                   _stream(stream)), "lkv_init_compose")
+
+
+def gdn_chunk_scan(layer: Layer, online: Tokens, scale: float, S_init: Optional[torch.Tensor],
+                   o: Optional[torch.Tensor], S_final: Optional[torch.Tensor], stream=None) -> None:
+    _check(load().lkv_gdn_chunk_scan(ctypes.byref(layer), ctypes.byref(online), float(scale), _ptr(S_init),
+                                     _ptr(o), _ptr(S_final), _stream(stream)), "lkv_gdn_chunk_scan")
+
+
+def ssd_chunk_scan(layer: Layer, online: Tokens, S_init: Optional[torch.Tensor], y: Optional[torch.Tensor],
+                   S_final: Optional[torch.Tensor], stream=None) -> None:
+    _check(load().lkv_ssd_chunk_scan(ctypes.byref(layer), ctypes.byref(online), _ptr(S_init), _ptr(y),
+                                     _ptr(S_final), _stream(stream)), "lkv_ssd_chunk_scan")

@@ -1,0 +1,88 @@
+"""CPU-side checks of the C ABI: the library loads, exports every symbol the
+header declares, and rejects bad arguments synchronously (no GPU needed: all
+of these return before any HIP call)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lkv.h")
+LIB = os.path.join(ROOT, "paper_2608_11231_amd", "liblkv.so")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(LIB), reason="liblkv.so not built")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(lkv_[a-z_0-9]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2608_11231_amd import lkv
+    return lkv.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _declared()
+    assert {"lkv_block_summary", "lkv_init_single", "lkv_init_compose", "lkv_gdn_chunk_scan",
+            "lkv_ssd_chunk_scan"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+    from paper_2608_11231_amd import lkv
+    assert set(names) == set(lkv.EXPORTS)
+
+
+def test_version_and_strings(lib):
+    assert lib.lkv_abi_version() == 1
+    assert lib.lkv_status_string(0) == b"ok"
+    assert b"NULL" in lib.lkv_status_string(1)
+
+
+def _layer(**kw):
+    from paper_2608_11231_amd import lkv
+    d = dict(family=0, h_qk=2, h_v=4, dk=128, dv=128, chunk=64, io_dtype=1, gate_dtype=1)
+    d.update(kw)
+    return lkv.Layer(**d)
+
+
+def _tokens(n_seq=0, n_tok=0):
+    from paper_2608_11231_amd import lkv
+    t = lkv.Tokens()
+    t.n_seq, t.n_tok = n_seq, n_tok
+    return t
+
+
+def test_argument_validation(lib):
+    by = ctypes.byref
+    T = _tokens()
+    assert lib.lkv_gdn_chunk_scan(None, by(T), ctypes.c_float(1.0), None, None, None, None) == 1
+    assert lib.lkv_gdn_chunk_scan(by(_layer(dk=96)), by(T), ctypes.c_float(1.0), None, None, None, None) == 5
+    assert lib.lkv_gdn_chunk_scan(by(_layer(dv=40)), by(T), ctypes.c_float(1.0), None, None, None, None) == 5
+    assert lib.lkv_gdn_chunk_scan(by(_layer(chunk=48)), by(T), ctypes.c_float(1.0), None, None, None, None) == 5
+    assert lib.lkv_gdn_chunk_scan(by(_layer(h_v=3)), by(T), ctypes.c_float(1.0), None, None, None, None) == 2
+    assert lib.lkv_gdn_chunk_scan(by(_layer(io_dtype=7)), by(T), ctypes.c_float(1.0), None, None, None, None) == 3
+    # family mismatch
+    assert lib.lkv_ssd_chunk_scan(by(_layer()), by(T), None, None, None, None) == 2
+    assert lib.lkv_ssd_chunk_scan(by(_layer(family=1, gate_dtype=1)), by(T), None, None, None, None) == 3
+    # empty batch: nothing to launch
+    assert lib.lkv_gdn_chunk_scan(by(_layer()), by(T), ctypes.c_float(1.0), None, None, None, None) == 0
+    # missing token tensors
+    T2 = _tokens(1, 10)
+    T2.cu = ctypes.c_void_p(0x1000)
+    assert lib.lkv_gdn_chunk_scan(by(_layer()), by(T2), ctypes.c_float(1.0), None, None, None, None) == 1
+    # misaligned tensor
+    T3 = _tokens(1, 10)
+    T3.cu = T3.k = T3.v = T3.g = T3.beta = T3.q = ctypes.c_void_p(0x1008)
+    assert lib.lkv_gdn_chunk_scan(by(_layer()), by(T3), ctypes.c_float(1.0), None, None, None, None) == 4
+    # summaries need at least one output
+    assert lib.lkv_block_summary(by(_layer()), by(T), None, None, None) == 1
+    # init calls
+    assert lib.lkv_init_single(by(_layer()), -1, 1, None, None, None, None) == 2
+    assert lib.lkv_init_single(by(_layer()), 0, 1, None, None, None, None) == 0
+    assert lib.lkv_init_single(by(_layer()), 2, 1, None, None, None, None) == 1
+    assert lib.lkv_init_compose(by(_layer()), 1, 1, None, None, None, None, 0, None, None) == 1
+    assert lib.lkv_init_compose(by(_layer()), 0, 0, None, None, None, None, 0, None, None) == 0
