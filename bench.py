@@ -1,0 +1,291 @@
+#!/usr/bin/env python3
+"""Benchmark of one recurrent layer's online prefill on one MI355X.
+
+One step is one pass of the whole hot path over one batch of synthetic input
+already resident in HBM:
+  1. lkv_init_single   -- LinearKV's single-block initial state (last block),
+  2. lkv_block_summary -- online fold of every cached block's transition M_k
+                          (the exact-composition mode's extra work),
+  3. lkv_init_compose  -- exact composition of the K cached (M_k, B_k) pairs,
+  4. the chunk scan    -- Gated DeltaNet (or Mamba-2) recurrence over the online
+                          tokens from the composed state, with outputs.
+The per-block states B_k are the cache's content (computed offline in the
+paper), so they are built once before timing.
+
+Prints ONE JSON line.  ``value`` = online tokens / step time.  Per-kernel
+durations come from HIP events on the stream the library launches on, inside
+the timed region; ``roofline`` is given for the kernel that takes the most time
+and ``roofline_by_kernel`` for all four.  ``cpu_baseline`` times the CPU oracle
+on a bounded sample of the same workload and scales it to the whole step.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 MFMA
+RIDGE = MFMA_BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+# ---------------------------------------------------------------- algorithmic work
+def work_model(w):
+    """Algorithmic bytes and flops per launch of each kernel of the step.
+
+    Bytes count every tensor the call must touch exactly once (q/k per q/k head,
+    v/g/beta per value head, outputs written once).  Flops are the chunkwise
+    minimum (matrix products of the chunk form, the triangular solve as C^3/3);
+    the extra bf16 hi/lo passes the kernels issue for fp32 accuracy are not
+    counted.
+    """
+    L = w.layer
+    io = 2 if L.io_dtype == "bf16" else 4
+    gb = 2 if (L.gate_dtype == "bf16" and L.family == 0) else 4
+    C, dk, dv, hq, hv = L.chunk, L.dk, L.dv, L.h_qk, L.h_v
+    T = w.online.n_tok
+    Tc = w.cached.n_tok
+    n_req, n_blk = w.n_req, w.n_blk
+    state = n_req * hv * dv * dk * 4
+    n_gates = 2 if L.family == 0 else 1
+    out = {}
+    out["init_single"] = dict(bytes=2 * state, flops=0)
+    # scan
+    chunks = sum(-(-int(x) // C) for x in np.diff(w.online.cu))
+    if L.family == 0:
+        per_chunk = 5 * 2 * C * C * dk + 3 * 2 * C * dk * dv + C ** 3 / 3
+    else:
+        per_chunk = 2 * C * C * dk + 2 * C * C * dv + 2 * 2 * C * dk * dv
+    out["scan"] = dict(bytes=T * (2 * hq * dk * io + hv * dv * io * 2 + n_gates * hv * gb) + 2 * state,
+                       flops=chunks * hv * per_chunk)
+    # fold (transitions of every cached block)
+    if L.family == 0:
+        cchunks = sum(-(-int(x) // C) for x in np.diff(w.cached.cu))
+        per = 2 * C * C * dk + C ** 3 / 3 + 2 * C * dk * dk + 2 * C * C * dk + 2 * C * dk * dk
+        out["fold"] = dict(bytes=Tc * (hq * dk * io + 2 * hv * gb) + n_blk * hv * dk * dk * 4,
+                           flops=cchunks * hv * per)
+    else:
+        out["fold"] = dict(bytes=Tc * hv * 4 + n_blk * hv * 4, flops=Tc * hv)
+    # composition
+    K = np.diff(w.blk_cu)
+    n_trans = int(np.sum(np.maximum(K - 1, 0)))
+    if L.family == 0:
+        out["compose"] = dict(bytes=(n_blk * hv * dv * dk + n_trans * hv * dk * dk) * 4 + state,
+                              flops=n_trans * hv * 2 * dv * dk * dk)
+    else:
+        out["compose"] = dict(bytes=n_blk * hv * dv * dk * 4 + n_trans * hv * 4 + state,
+                              flops=n_trans * hv * 2 * dv * dk)
+    return out
+
+
+def roofline(name, work, ms):
+    secs = ms * 1e-3
+    ai = work["flops"] / max(work["bytes"], 1)
+    if ai > RIDGE:
+        ach = work["flops"] / secs / 1e12
+        return dict(kernel=name, bound="mfma", achieved=round(ach, 2), peak=MFMA_BF16_PEAK_TFLOPS,
+                    unit="TFLOP/s", frac=round(ach / MFMA_BF16_PEAK_TFLOPS, 4), traffic=None,
+                    avg_us=round(ms * 1e3, 2), algorithmic_flops=work["flops"],
+                    algorithmic_bytes=work["bytes"])
+    ach = work["bytes"] / secs / 1e9
+    return dict(kernel=name, bound="hbm", achieved=round(ach, 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                frac=round(ach / HBM_PEAK_GBS, 4), traffic=None, avg_us=round(ms * 1e3, 2),
+                algorithmic_flops=work["flops"], algorithmic_bytes=work["bytes"])
+
+
+# ---------------------------------------------------------------- CPU oracle baseline
+def cpu_baseline(w, budget_s: float):
+    """Time the fp64 CPU oracle on request 0 (all heads) and scale to the step."""
+    import oracle
+    from paper_2608_11231_amd import inputs as I
+    L = w.layer
+    gdn = L.family == I.GDN
+    cores = int(os.environ.get("OMP_NUM_THREADS", 0) or len(os.sched_getaffinity(0)))
+    oracle.load()
+    c, o = w.cached, w.online
+    b0, b1 = int(w.blk_cu[0]), int(w.blk_cu[1])
+    t0, t1 = int(c.cu[b0]), int(c.cu[b1])
+    # scan sample: request 0, every head
+    s0, s1 = int(o.cu[0]), int(o.cu[1])
+    cu = np.array([0, s1 - s0], np.int32)
+    S0 = np.zeros((1, L.h_v, L.dv, L.dk))
+    tic = time.perf_counter()
+    if gdn:
+        oracle.gdn_scan(cu, o.q[s0:s1], o.k[s0:s1], o.v[s0:s1], o.g[s0:s1], o.beta[s0:s1],
+                        scale=w.scale, S0=S0)
+    else:
+        oracle.ssd_scan(cu, o.q[s0:s1], o.k[s0:s1], o.v[s0:s1], o.g[s0:s1], w.A, S0=S0)
+    t_scan = time.perf_counter() - tic
+    # fold sample: request 0's blocks, as many as fit in the remaining budget
+    fold_blocks = []
+    est_per_tok = t_scan / max(s1 - s0, 1)
+    room = max(budget_s - 2 * t_scan, budget_s * 0.25)
+    tok = 0
+    for b in range(b0, b1):
+        L_b = int(c.cu[b + 1] - c.cu[b])
+        if fold_blocks and (tok + L_b) * est_per_tok > room:
+            break
+        fold_blocks.append(b)
+        tok += L_b
+    fb0, fb1 = fold_blocks[0], fold_blocks[-1] + 1
+    ft0, ft1 = int(c.cu[fb0]), int(c.cu[fb1])
+    fcu = (c.cu[fb0:fb1 + 1] - c.cu[fb0]).astype(np.int32)
+    tic = time.perf_counter()
+    if gdn:
+        oracle.gdn_transition(fcu, c.k[ft0:ft1], c.g[ft0:ft1], c.beta[ft0:ft1])
+    else:
+        oracle.ssd_log_decay(fcu, c.g[ft0:ft1], w.A)
+    t_fold = time.perf_counter() - tic
+    # compose sample: request 0 on synthetic pools of the real shapes
+    K0 = b1 - b0
+    rng = np.random.default_rng(0)
+    Bp = rng.standard_normal((K0, L.h_v, L.dv, L.dk))
+    Mp = rng.standard_normal((K0, L.h_v, L.dk, L.dk)) / np.sqrt(L.dk) if gdn else \
+        -rng.uniform(0, 1, (K0, L.h_v))
+    ids = np.arange(K0, dtype=np.int32)
+    tic = time.perf_counter()
+    (oracle.compose_gdn if gdn else oracle.compose_ssd)(np.array([0, K0], np.int32), ids, Bp, Mp)
+    t_comp = time.perf_counter() - tic
+    tic = time.perf_counter()
+    oracle.init_single(Bp, np.array([K0 - 1], np.int32))
+    t_single = time.perf_counter() - tic
+    # scale each op to the whole batch by its units of work
+    T_all = w.online.n_tok
+    n_trans_all = int(np.sum(np.maximum(np.diff(w.blk_cu) - 1, 0)))
+    step = (t_scan * T_all / (s1 - s0) + t_fold * w.cached.n_tok / (ft1 - ft0)
+            + t_comp * n_trans_all / max(K0 - 1, 1) + t_single * w.n_req)
+    sample = (f"request 0 of {w.n_req}, all {L.h_v} heads: scan of {s1 - s0} online tokens "
+              f"({t_scan:.2f} s), transition fold of {len(fold_blocks)} cached blocks / {ft1 - ft0} tokens "
+              f"({t_fold:.2f} s), {K0}-block composition ({t_comp:.2f} s), single init; scaled by "
+              f"tokens / transitions / requests to the whole step")
+    return dict(value=round(T_all / step, 1), unit="tokens/s", cores=cores, kind="oracle", sample=sample,
+                step_s_extrapolated=round(step, 3))
+
+
+# ---------------------------------------------------------------- main
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=3,
+                    help="workload index (default 3: Gated DeltaNet, 32K context, 4 requests)")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
+    ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of CPU-oracle work")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="after timing, run a plain 512 MiB device copy (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build measures one GPU only (the hot path is per-GPU; see the "
+              "sharding note in the design document); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2608_11231_amd import gpu_io
+    from paper_2608_11231_amd import inputs as I
+
+    torch.cuda.set_device(0)
+    tic = time.perf_counter()
+    w = I.config(args.config, workers=16)
+    log(f"[bench] workload {w.name}: {w.online.n_tok} online tokens, {w.cached.n_tok} cached tokens in "
+        f"{w.n_blk} blocks, generated in {time.perf_counter() - tic:.1f} s")
+    G = gpu_io.GpuWorkload(w)
+    G.block_summary(B=True, M=False)        # the cache content: per-block states
+    torch.cuda.synchronize()
+    log("[bench] inputs resident in HBM; block states built")
+
+    ops = [("init_single", G.init_single),
+           ("fold", lambda: G.block_summary(B=False, M=True)),
+           ("compose", G.init_compose),
+           ("scan", lambda: G.scan(G.S_exact))]
+
+    def step(events=None):
+        for i, (_, f) in enumerate(ops):
+            if events is not None:
+                events[i][0].record()
+            f()
+            if events is not None:
+                events[i][1].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ev = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)] for _ in ops]
+          for _ in range(args.steps)]
+    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record()
+    for k in range(args.steps):
+        step(ev[k])
+    t_end.record()
+    torch.cuda.synchronize()
+    ms_step = t_start.elapsed_time(t_end) / args.steps
+    per_op = {name: float(np.mean([ev[k][i][0].elapsed_time(ev[k][i][1]) for k in range(args.steps)]))
+              for i, (name, _) in enumerate(ops)}
+    log("[bench] timed: " + ", ".join(f"{k} {v * 1e3:.1f} us" for k, v in per_op.items()))
+
+    if args.copy_probe:
+        src = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+
+    T = w.online.n_tok
+    work = work_model(w)
+    roofs = {name: roofline(name, work[name], per_op[name]) for name in per_op}
+    dominant = max(per_op, key=per_op.get)
+    L = w.layer
+    result = {
+        "metric": "online linear-layer prefill tokens/s at 8K/32K; K-way composition latency (us)",
+        "value": round(T / (ms_step * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{w.name}: {'Gated DeltaNet' if L.family == I.GDN else 'Mamba-2 SSD'} layer, "
+                         f"{w.n_req} requests x {T // max(w.n_req, 1)} online tokens, {L.h_v} heads, "
+                         f"dk={L.dk}, dv={L.dv}, chunk {L.chunk}, {w.n_blk} cached blocks "
+                         f"({w.cached.n_tok} tokens), bf16 inputs, fp32 state"),
+            "online_tokens": T,
+            "cached_tokens": w.cached.n_tok,
+            "cached_blocks": w.n_blk,
+            "requests": w.n_req,
+            "parallelism": "single GPU",
+        },
+        "composition_latency_us": round(per_op["compose"] * 1e3, 2),
+        "fold_plus_compose_latency_us": round((per_op["fold"] + per_op["compose"]) * 1e3, 2),
+        "single_init_latency_us": round(per_op["init_single"] * 1e3, 2),
+        "scan_us": round(per_op["scan"] * 1e3, 2),
+        "lb_tokens_per_s": round(T / ((per_op["init_single"] + per_op["scan"]) * 1e-3), 1),
+        "ex_tokens_per_s": round(T / ((per_op["fold"] + per_op["compose"] + per_op["scan"]) * 1e-3), 1),
+        "roofline": roofs[dominant],
+        "roofline_by_kernel": roofs,
+        "cpu_baseline": None,
+    }
+    if args.copy_probe:
+        result["copy_probe_bytes"] = 2 * (512 << 20)
+    if not args.no_cpu:
+        result["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -42,11 +42,11 @@ int env_int(const char* name, int dflt) {
 // Waves per workgroup for the chunk kernels: 16*nw state rows per workgroup.
 // More waves share the token x token work of a chunk; fewer waves give more
 // workgroups.  Pick the largest nw that still fills the 256 CUs.
-int pick_nw(int fam, int dk, int chunk, bool f32io, int64_t pairs, int rows, int rows2) {
+int pick_nw(int fam, int dk, int chunk, bool f32io, int64_t pairs, int rows, int rows2, bool summary) {
     int forced = env_int("LKV_SCAN_NW", 0);
     for (int nw = 4; nw >= 1; nw >>= 1) {
         if (rows % (16 * nw) || (rows2 && rows2 % (16 * nw))) continue;
-        if (scan_lds_bytes(fam, dk, chunk, f32io, nw) > 160 * 1024) continue;
+        if (scan_lds_bytes(fam, dk, chunk, f32io, nw, summary) > 160 * 1024) continue;
         if (forced) {
             if (nw == forced) return nw;
             continue;
@@ -106,7 +106,7 @@ lkv_status chunk_scan(const lkv_layer* L, const lkv_tokens* T, float scale, cons
     if (!out && !S_final) return LKV_OK;
     const bool f32io = L->io_dtype == LKV_F32;
     const int64_t pairs = (int64_t)T->n_seq * L->h_v;
-    const int nw = pick_nw(L->family, L->dk, L->chunk, f32io, pairs, L->dv, 0);
+    const int nw = pick_nw(L->family, L->dk, L->chunk, f32io, pairs, L->dv, 0, false);
     const int64_t units = pairs * (L->dv / (16 * nw));
     if (units >= (INT64_C(1) << 31)) return LKV_E_SHAPE;
     ScanArgs a = base_args(L, T);
@@ -174,7 +174,7 @@ lkv_status lkv_block_summary(const lkv_layer* L, const lkv_tokens* T, float* B_o
         return hip_status(launch_scan(L, a, st));
     }
     const int nw = pick_nw(L->family, L->dk, L->chunk, f32io, pairs, rows_b ? rows_b : rows_m,
-                           rows_b ? rows_m : 0);
+                           rows_b ? rows_m : 0, true);
     a.nw = nw;
     a.tiles_b = rows_b / (16 * nw);
     a.tiles_m = rows_m / (16 * nw);

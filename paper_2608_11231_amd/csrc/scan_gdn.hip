@@ -22,9 +22,10 @@ namespace lkv {
 
 #define LKV_LDS(FAM_, DK_, CH_)                                                            \
     if (dk == DK_ && chunk == CH_)                                                          \
-        return f32io ? ScanLds<FAM_, DK_, CH_, true>::bytes(nw) : ScanLds<FAM_, DK_, CH_, false>::bytes(nw);
+        return f32io ? scan_lds_t<FAM_, DK_, CH_, true>(nw, summary)                       \
+                     : scan_lds_t<FAM_, DK_, CH_, false>(nw, summary);
 
-size_t scan_lds_bytes(int fam, int dk, int chunk, bool f32io, int nw) {
+size_t scan_lds_bytes(int fam, int dk, int chunk, bool f32io, int nw, bool summary) {
     if (fam == FAM_GDN) {
         LKV_LDS(FAM_GDN, 16, 16) LKV_LDS(FAM_GDN, 32, 16) LKV_LDS(FAM_GDN, 64, 16) LKV_LDS(FAM_GDN, 128, 16)
         LKV_LDS(FAM_GDN, 16, 64) LKV_LDS(FAM_GDN, 32, 64) LKV_LDS(FAM_GDN, 64, 64) LKV_LDS(FAM_GDN, 128, 64)

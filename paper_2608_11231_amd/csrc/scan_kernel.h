@@ -2,9 +2,9 @@
 // used by lkv_gdn_chunk_scan / lkv_ssd_chunk_scan (online prefill) and by
 // lkv_block_summary (per-block state from zero and per-block transition).
 //
-// Work unit = (segment s, value head h, row tile).  A row tile is 16*nw rows
+// Work unit = (segment s, value head h, row tile).  A row tile is 16*NW rows
 // of the dv x dk state (rows of a state evolve independently: the transition
-// acts on the dk side only), so a workgroup of nw waves owns 16*nw state rows
+// acts on the dk side only), so a workgroup of NW waves owns 16*NW state rows
 // and each wave owns 16 of them.  Chunks of CH tokens are processed in order;
 // the fp32 state never leaves registers between chunks.
 //
@@ -61,21 +61,21 @@ struct ScanArgs {
     int32_t n_units;
 };
 
-template <int FAM, int DK, int CH, bool F32IO>
+template <int FAM, int DK, int CH, bool F32IO, int NW>
 struct ScanLds {
+    // Layout: [K | K^T | L | N | gates | per-wave gate prefix | V^T | Q | P].  The
+    // block-summary mode has no outputs and stops before Q, so it needs less LDS
+    // and fits more workgroups per CU.
     static constexpr int NTC = CH / 16;
     static constexpr int SK = DK + 8;   // bf16 stride of [tok][dk] rows
     static constexpr int SC = CH + 8;   // bf16 stride of [*][tok] rows
     static constexpr int SCF = CH + 4;  // f32 stride of [tok][tok] rows
     static constexpr int SN = 20;       // f32 stride of a 16x16 block
     static constexpr int PL = F32IO ? 2 : 1;
-    static constexpr int PP = F32IO ? 2 : 1;  // planes of P
     static __host__ __device__ constexpr size_t al(size_t x) { return (x + 15) & ~size_t(15); }
     static __host__ __device__ constexpr size_t k_off() { return 0; }
     static __host__ __device__ constexpr size_t kt_off() { return al(k_off() + size_t(PL) * CH * SK * 2); }
-    static __host__ __device__ constexpr size_t q_off() { return al(kt_off() + size_t(PL) * DK * SC * 2); }
-    static __host__ __device__ constexpr size_t p_off() { return al(q_off() + size_t(PL) * CH * SK * 2); }
-    static __host__ __device__ constexpr size_t l_off() { return al(p_off() + size_t(PP) * CH * SC * 2); }
+    static __host__ __device__ constexpr size_t l_off() { return al(kt_off() + size_t(PL) * DK * SC * 2); }
     static __host__ __device__ constexpr size_t n_off() {
         return al(l_off() + (FAM == FAM_GDN ? size_t(CH) * SCF * 4 : 0));
     }
@@ -84,10 +84,11 @@ struct ScanLds {
     }
     static __host__ __device__ constexpr size_t be_off() { return al(gr_off() + CH * 4); }
     static __host__ __device__ constexpr size_t gc_off() { return al(be_off() + CH * 4); }
-    static __host__ __device__ constexpr size_t vt_off() { return al(gc_off() + 4 * 64 * 4); }
-    static __host__ __device__ constexpr size_t bytes(int nw) {
-        return al(vt_off() + size_t(PL) * 16 * nw * SC * 2);
-    }
+    static __host__ __device__ constexpr size_t vt_off() { return al(gc_off() + NW * 64 * 4); }
+    static __host__ __device__ constexpr size_t q_off() { return al(vt_off() + size_t(PL) * 16 * NW * SC * 2); }
+    static __host__ __device__ constexpr size_t p_off() { return al(q_off() + size_t(PL) * CH * SK * 2); }
+    static __host__ __device__ constexpr size_t end_off() { return al(p_off() + size_t(PL) * CH * SC * 2); }
+    static __host__ __device__ constexpr size_t bytes(bool summary) { return summary ? q_off() : end_off(); }
 };
 
 // acc += A(rows of an LDS matrix, 16-slices [kb, ke)) x B(acc-layout tiles)
@@ -185,60 +186,69 @@ __device__ __forceinline__ float load_gate(const void* p, int64_t idx, bool is_b
                    : reinterpret_cast<const float*>(p)[idx];
 }
 
-// Stage a [CH x ncols] token-major tile into LDS (element (t, c) of the source
-// at off + t*row_stride + c): row-major copy at `dst`
-// (stride ds, if non-null) and/or transposed copy at `dstT` (stride dts,
-// dstT[c][t]).  Rows t >= n are zero.  F32IO splits into two planes (plane
-// offsets pofs / pofsT elements).
-template <int CH, bool F32IO>
-__device__ __forceinline__ void stage_tile(const void* src, int64_t off, int n, int64_t row_stride,
-                                           int ncols, bf16* dst, int ds, int pofs, bf16* dstT,
-                                           int dts, int pofsT, int tid, int nthreads) {
-    if (!F32IO) {
-        const int vpr = ncols / 8;  // 16-byte vectors per row
-        const bf16* s = reinterpret_cast<const bf16*>(src);
-        for (int idx = tid; idx < CH * vpr; idx += nthreads) {
-            const int t = idx / vpr, c = (idx % vpr) * 8;
-            bf16x8 x;
-            if (t < n) {
-                x = *reinterpret_cast<const bf16x8*>(s + off + t * row_stride + c);
-            } else {
+// A [CH x NCOL] token-major tile of a global tensor, prefetched into registers
+// (16-byte vectors, spread over the NTH threads of the workgroup) and later
+// committed to LDS as a row-major copy and/or a transposed copy.  Rows t >= n
+// read as zero.  The prefetch of chunk c+1 is issued right after chunk c is
+// committed, so its latency overlaps chunk c's arithmetic.
+template <int CH, int NCOL, bool F32IO, int NTH>
+struct TileRegs {
+    static constexpr int EPV = F32IO ? 4 : 8;           // elements per 16-byte vector
+    static constexpr int VPR = NCOL / EPV;               // vectors per row
+    static constexpr int NV = CH * VPR;                  // vectors per tile
+    static constexpr int PER = (NV + NTH - 1) / NTH;     // vectors per thread
+    uint4 r[PER];
+
+    // element (t, c) of the source lives at base + t*row_stride + c (elements)
+    __device__ __forceinline__ void load(const void* base, int64_t row_stride, int n, int tid) {
+        constexpr int ES = F32IO ? 4 : 2;
+        const char* b = reinterpret_cast<const char*>(base);
 #pragma unroll
-                for (int e = 0; e < 8; ++e) x[e] = (bf16)0.f;
-            }
-            if (dst) *reinterpret_cast<bf16x8*>(dst + t * ds + c) = x;
-            if (dstT) {
-#pragma unroll
-                for (int e = 0; e < 8; ++e) dstT[(c + e) * dts + t] = x[e];
-            }
+        for (int i = 0; i < PER; ++i) {
+            const int idx = tid + i * NTH;
+            const int t = idx / VPR, c = (idx % VPR) * EPV;
+            uint4 x = uint4{0u, 0u, 0u, 0u};
+            if (idx < NV && t < n) x = *reinterpret_cast<const uint4*>(b + (t * row_stride + c) * ES);
+            r[i] = x;
         }
-    } else {
-        const int vpr = ncols / 4;
-        const float* s = reinterpret_cast<const float*>(src);
-        for (int idx = tid; idx < CH * vpr; idx += nthreads) {
-            const int t = idx / vpr, c = (idx % vpr) * 4;
-            f32x4 x = zero4();
-            if (t < n) x = *reinterpret_cast<const f32x4*>(s + off + t * row_stride + c);
-            const Split4 sp = split4(x);
-            if (dst) {
-                *reinterpret_cast<bf16x4*>(dst + t * ds + c) = sp.hi;
-                *reinterpret_cast<bf16x4*>(dst + pofs + t * ds + c) = sp.lo;
-            }
-            if (dstT) {
+    }
+    // dst (stride ds, plane offset pofs) and/or dstT[c][t] (stride dts, plane offset pofsT)
+    __device__ __forceinline__ void commit(bf16* dst, int ds, int pofs, bf16* dstT, int dts, int pofsT,
+                                           int tid) const {
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    dstT[(c + e) * dts + t] = sp.hi[e];
-                    dstT[pofsT + (c + e) * dts + t] = sp.lo[e];
+        for (int i = 0; i < PER; ++i) {
+            const int idx = tid + i * NTH;
+            if (idx >= NV) continue;
+            const int t = idx / VPR, c = (idx % VPR) * EPV;
+            if (!F32IO) {
+                const bf16x8 x = __builtin_bit_cast(bf16x8, r[i]);
+                if (dst) *reinterpret_cast<bf16x8*>(dst + t * ds + c) = x;
+                if (dstT) {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) dstT[(c + e) * dts + t] = x[e];
+                }
+            } else {
+                const Split4 sp = split4(__builtin_bit_cast(f32x4, r[i]));
+                if (dst) {
+                    *reinterpret_cast<bf16x4*>(dst + t * ds + c) = sp.hi;
+                    *reinterpret_cast<bf16x4*>(dst + pofs + t * ds + c) = sp.lo;
+                }
+                if (dstT) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        dstT[(c + e) * dts + t] = sp.hi[e];
+                        dstT[pofsT + (c + e) * dts + t] = sp.lo[e];
+                    }
                 }
             }
         }
     }
-}
+};
 
-template <int FAM, int DK, int CH, bool F32IO>
-__global__ __launch_bounds__(256) void scan_kernel(ScanArgs p) {
-    using Ly = ScanLds<FAM, DK, CH, F32IO>;
-    constexpr int NTC = CH / 16, NTK = DK / 16;
+template <int FAM, int DK, int CH, bool F32IO, int NW>
+__global__ __launch_bounds__(64 * NW) void scan_kernel(ScanArgs p) {
+    using Ly = ScanLds<FAM, DK, CH, F32IO, NW>;
+    constexpr int NTC = CH / 16, NTK = DK / 16, NTH = 64 * NW;
     constexpr int SK = Ly::SK, SC = Ly::SC, SCF = Ly::SCF, SN = Ly::SN;
     extern __shared__ __align__(16) char smem[];
     bf16* sK = reinterpret_cast<bf16*>(smem + Ly::k_off());
@@ -251,16 +261,14 @@ __global__ __launch_bounds__(256) void scan_kernel(ScanArgs p) {
     float* sBe = reinterpret_cast<float*>(smem + Ly::be_off());
     float* sGcAll = reinterpret_cast<float*>(smem + Ly::gc_off());
     bf16* sVT = reinterpret_cast<bf16*>(smem + Ly::vt_off());
-    constexpr int KPL = CH * SK;   // plane offset of sK / sQ
-    constexpr int KTPL = DK * SC;  // plane offset of sKT
-    constexpr int PPL = CH * SC;   // plane offset of sP
+    constexpr int KPL = CH * SK;       // plane offset of sK / sQ
+    constexpr int KTPL = DK * SC;      // plane offset of sKT
+    constexpr int PPL = CH * SC;       // plane offset of sP
+    constexpr int VTPL = 16 * NW * SC;  // plane offset of sVT
 
-    const int nw = p.nw;
-    const int nthreads = 64 * nw;
     const int tid = threadIdx.x;
     const int w = tid >> 6, lane = tid & 63, g = lane >> 4, c16 = lane & 15;
     float* sGc = sGcAll + 64 * w;
-    const int VTPL = 16 * nw * SC;  // plane offset of sVT
 
     // ---- work unit
     const int tiles = p.tiles_b + p.tiles_m;
@@ -269,7 +277,7 @@ __global__ __launch_bounds__(256) void scan_kernel(ScanArgs p) {
     const int h = (u / tiles) % p.h_v;
     const int s = u / (tiles * p.h_v);
     const bool mtile = tile >= p.tiles_b;
-    const int row0 = (mtile ? tile - p.tiles_b : tile) * 16 * nw;
+    const int row0 = (mtile ? tile - p.tiles_b : tile) * 16 * NW;
     const int my_row = row0 + 16 * w + c16;
     const int hq = h / (p.h_v / p.h_qk);
     int64_t t0 = p.cu[s], t1 = p.cu[s + 1];
@@ -293,31 +301,45 @@ __global__ __launch_bounds__(256) void scan_kernel(ScanArgs p) {
     }
     float lam_sum = 0.f;
 
+    // ---- global -> register prefetch of one chunk
+    TileRegs<CH, DK, F32IO, NTH> pk, pq;
+    TileRegs<CH, 16 * NW, F32IO, NTH> pv;
+    float pg = 0.f, pb = 0.f;
+    const int64_t qk_rs = (int64_t)p.h_qk * DK, v_rs = (int64_t)p.h_v * p.dv;
+    auto prefetch = [&](int64_t c0) {
+        const int n = (int)((t1 - c0) < CH ? (t1 - c0) : CH);
+        const int64_t qk_off = (c0 * p.h_qk + hq) * (int64_t)DK;
+        const int es = F32IO ? 4 : 2;
+        pk.load(reinterpret_cast<const char*>(p.k) + qk_off * es, qk_rs, n, tid);
+        if (with_out) pq.load(reinterpret_cast<const char*>(p.q) + qk_off * es, qk_rs, n, tid);
+        if (load_v) pv.load(reinterpret_cast<const char*>(p.v) + ((c0 * p.h_v + h) * (int64_t)p.dv + row0) * es,
+                            v_rs, n, tid);
+        if (tid < CH) {
+            const int64_t gi = (c0 + tid) * p.h_v + h;
+            if (FAM == FAM_GDN) {
+                pg = tid < n ? load_gate(p.g, gi, p.gate_bf16) : 0.f;
+                pb = tid < n ? load_gate(p.beta, gi, p.gate_bf16) : 0.f;
+            } else {
+                const float dt = tid < n ? reinterpret_cast<const float*>(p.g)[gi] : 0.f;
+                pg = Ah * dt;
+                pb = dt;
+            }
+        }
+    };
+    if (t0 < t1) prefetch(t0);
+
     for (int64_t c0 = t0; c0 < t1; c0 += CH) {
         const int n = (int)((t1 - c0) < CH ? (t1 - c0) : CH);
         __syncthreads();  // previous chunk is done with LDS
-        // ---- stage inputs
-        const int64_t qk_off = (c0 * p.h_qk + hq) * (int64_t)DK, qk_rs = (int64_t)p.h_qk * DK;
-        stage_tile<CH, F32IO>(p.k, qk_off, n, qk_rs, DK, sK, SK, KPL, sKT, SC, KTPL, tid, nthreads);
-        if (with_out)
-            stage_tile<CH, F32IO>(p.q, qk_off, n, qk_rs, DK, sQ, SK, KPL, nullptr, 0, 0, tid, nthreads);
-        if (load_v) {
-            // v rows: element (tok, row0 + c) at ((tok * h_v + h) * dv + row0 + c)
-            const int64_t base = (c0 * p.h_v + h) * (int64_t)p.dv + row0;
-            stage_tile<CH, F32IO>(p.v, base, n, (int64_t)p.h_v * p.dv, 16 * nw, nullptr, 0, 0, sVT, SC,
-                                  VTPL, tid, nthreads);
+        // ---- commit the prefetched chunk to LDS, then start fetching the next one
+        pk.commit(sK, SK, KPL, sKT, SC, KTPL, tid);
+        if (with_out) pq.commit(sQ, SK, KPL, nullptr, 0, 0, tid);
+        if (load_v) pv.commit(nullptr, 0, 0, sVT, SC, VTPL, tid);
+        if (tid < CH) {
+            sGr[tid] = pg;
+            sBe[tid] = pb;
         }
-        for (int t = tid; t < CH; t += nthreads) {
-            const int64_t gi = (c0 + t) * p.h_v + h;
-            if (FAM == FAM_GDN) {
-                sGr[t] = t < n ? load_gate(p.g, gi, p.gate_bf16) : 0.f;
-                sBe[t] = t < n ? load_gate(p.beta, gi, p.gate_bf16) : 0.f;
-            } else {
-                const float dt = t < n ? reinterpret_cast<const float*>(p.g)[gi] : 0.f;
-                sGr[t] = Ah * dt;
-                sBe[t] = dt;
-            }
-        }
+        if (c0 + CH < t1) prefetch(c0 + CH);
         __syncthreads();
 
         // ---- in-chunk cumulative log-gate (every wave keeps its own copy)
@@ -331,7 +353,7 @@ __global__ __launch_bounds__(256) void scan_kernel(ScanArgs p) {
         if (FAM == FAM_GDN || with_out) {
             constexpr int NPAIR = NTC * (NTC + 1) / 2;
             const int nprod = (FAM == FAM_GDN) ? (with_out ? 2 : 1) : 1;
-            for (int item = w; item < nprod * NPAIR; item += nw) {
+            for (int item = w; item < nprod * NPAIR; item += NW) {
                 const int which = item / NPAIR;  // GDN: 0 = K K^T, 1 = Q K^T; SSD: 0 = C B^T
                 int pi = item % NPAIR, mt = 0;
                 while (pi > mt) { pi -= mt + 1; ++mt; }
@@ -362,8 +384,8 @@ __global__ __launch_bounds__(256) void scan_kernel(ScanArgs p) {
             if (FAM == FAM_GDN) {
                 __syncthreads();
                 // inverse of each 16x16 diagonal block of (I + L): wave w, lane group
-                // g handles block w + nw*g, lane c16 computes column c16
-                const int b = w + nw * g;
+                // g handles block w + NW*g, lane c16 computes column c16
+                const int b = w + NW * g;
                 if (b < NTC) {
                     float x[16];
                     const float* Lb = sL + (16 * b) * SCF + 16 * b;
@@ -501,17 +523,37 @@ __global__ __launch_bounds__(256) void scan_kernel(ScanArgs p) {
 
 hipError_t launch_scan_gdn(int dk, int chunk, bool f32io, const ScanArgs& a, hipStream_t st);
 hipError_t launch_scan_ssd(int dk, int chunk, bool f32io, const ScanArgs& a, hipStream_t st);
-size_t scan_lds_bytes(int fam, int dk, int chunk, bool f32io, int nw);
+size_t scan_lds_bytes(int fam, int dk, int chunk, bool f32io, int nw, bool summary);
 
-template <int FAM, int DK, int CH, bool F32IO>
-hipError_t launch_scan_t(const ScanArgs& a, hipStream_t st) {
-    const size_t lds = ScanLds<FAM, DK, CH, F32IO>::bytes(a.nw);
-    auto kern = scan_kernel<FAM, DK, CH, F32IO>;
+template <int FAM, int DK, int CH, bool F32IO, int NW>
+hipError_t launch_scan_nw(const ScanArgs& a, hipStream_t st) {
+    const size_t lds = ScanLds<FAM, DK, CH, F32IO, NW>::bytes(a.summary != 0);
+    auto kern = scan_kernel<FAM, DK, CH, F32IO, NW>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kern, dim3(a.n_units), dim3(64 * a.nw), lds, st, a);
+    hipLaunchKernelGGL(kern, dim3(a.n_units), dim3(64 * NW), lds, st, a);
     return hipGetLastError();
+}
+
+template <int FAM, int DK, int CH, bool F32IO>
+hipError_t launch_scan_t(const ScanArgs& a, hipStream_t st) {
+    switch (a.nw) {
+        case 1: return launch_scan_nw<FAM, DK, CH, F32IO, 1>(a, st);
+        case 2: return launch_scan_nw<FAM, DK, CH, F32IO, 2>(a, st);
+        case 4: return launch_scan_nw<FAM, DK, CH, F32IO, 4>(a, st);
+    }
+    return hipErrorInvalidValue;
+}
+
+template <int FAM, int DK, int CH, bool F32IO>
+size_t scan_lds_t(int nw, bool summary) {
+    switch (nw) {
+        case 1: return ScanLds<FAM, DK, CH, F32IO, 1>::bytes(summary);
+        case 2: return ScanLds<FAM, DK, CH, F32IO, 2>::bytes(summary);
+        case 4: return ScanLds<FAM, DK, CH, F32IO, 4>::bytes(summary);
+    }
+    return 0;
 }
 
 }  // namespace lkv

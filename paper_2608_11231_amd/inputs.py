@@ -326,7 +326,7 @@ def config(index: int, seed: Optional[int] = None, mild: bool = False,
         law = GateLaw(x_mu=-9.0, beta_mu=-4.0) if mild else GateLaw()
         return build_workload(name, layer, [[1024] * 8], [1536], law, s, workers=workers)
     if index == 2:
-        layer = Layer(SSD, 1, 64, 128, 64, 64)
+        layer = Layer(SSD, 1, 64, 128, 64, 64, "bf16", "f32")
         law = GateLaw(dt_bias=-6.0) if mild else GateLaw()
         return build_workload(name, layer, [[1024] * 8], [1536], law, s, workers=workers)
     if index == 3:
