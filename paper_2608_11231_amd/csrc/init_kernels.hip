@@ -97,8 +97,9 @@ hipError_t launch_compose_ssd(int32_t n_req, int32_t n_blk, int32_t H, int64_t p
 // row0 + 16w + (lane % 16).  The state stays in registers in acc-tile layout
 // (tile nt: S[row][16nt + 4g + r]), which is directly the B operand of
 //   S_new^T = M^T S^T    (contraction over the state's dk index),
-// so each step needs only M^T staged in LDS, split into bf16 hi/lo planes
-// (products Mh*Sh + Mh*Sl + Ml*Sh keep the fp32 chain at ~1e-5 relative).
+// so each step stages only M in LDS (row-major, split into bf16 hi/lo planes;
+// products Mh*Sh + Mh*Sl + Ml*Sh keep the fp32 chain at ~1e-5 relative) and
+// reads the M^T fragments with transposed LDS loads.
 template <int DK>
 struct ComposeLds {
     static constexpr int SM = DK + 8;
@@ -136,17 +137,14 @@ __global__ __launch_bounds__(256) void compose_gdn_kernel(ComposeArgs p) {
             for (int nt = 0; nt < NTK; ++nt) S[nt] = *reinterpret_cast<const f32x4*>(Bj + 16 * nt);
             continue;
         }
-        // stage M^T (split) : sM[jj][ii] = M[ii][jj]
+        // stage M row-major, split into bf16 hi / lo planes (16-byte reads, 8-byte writes)
         const float* Mj = p.M_pool + ((int64_t)id * p.h_v + h) * DK * DK;
         __syncthreads();
         for (int idx = tid; idx < DK * DK / 4; idx += nthreads) {
             const int ii = idx / (DK / 4), jj = (idx % (DK / 4)) * 4;
             const Split4 sp = split4(*reinterpret_cast<const f32x4*>(Mj + ii * DK + jj));
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                sMh[(jj + e) * SM + ii] = sp.hi[e];
-                sMl[(jj + e) * SM + ii] = sp.lo[e];
-            }
+            *reinterpret_cast<bf16x4*>(sMh + ii * SM + jj) = sp.hi;
+            *reinterpret_cast<bf16x4*>(sMl + ii * SM + jj) = sp.lo;
         }
         __syncthreads();
         bf16x4 Sh[NTK], Sl[NTK];
@@ -156,22 +154,25 @@ __global__ __launch_bounds__(256) void compose_gdn_kernel(ComposeArgs p) {
             Sh[nt] = sp.hi;
             Sl[nt] = sp.lo;
         }
+        // S_new^T tile nt (rows j = 16nt..16nt+15) = M^T S^T: A fragments of M^T come
+        // straight from the row-major planes through transposed LDS reads
 #pragma unroll
         for (int nt = 0; nt < NTK; ++nt) {
-            const bf16* mh = sMh + (16 * nt + c16) * SM;
-            const bf16* ml = sMl + (16 * nt + c16) * SM;
             f32x4 acc = *reinterpret_cast<const f32x4*>(Bj + 16 * nt);
             int kg = 0;
 #pragma unroll
             for (; kg + 1 < NTK; kg += 2) {
-                const bf16x4 a0 = lds4(mh + 16 * kg + 4 * g), a1 = lds4(mh + 16 * kg + 16 + 4 * g);
-                const bf16x4 c0 = lds4(ml + 16 * kg + 4 * g), c1 = lds4(ml + 16 * kg + 16 + 4 * g);
+                const bf16x4 a0 = lds4_tr(sMh, SM, 16 * kg, 16 * nt, g, c16);
+                const bf16x4 a1 = lds4_tr(sMh, SM, 16 * kg + 16, 16 * nt, g, c16);
+                const bf16x4 c0 = lds4_tr(sMl, SM, 16 * kg, 16 * nt, g, c16);
+                const bf16x4 c1 = lds4_tr(sMl, SM, 16 * kg + 16, 16 * nt, g, c16);
                 acc = mma32(a0, a1, Sh[kg], Sh[kg + 1], acc);
                 acc = mma32(a0, a1, Sl[kg], Sl[kg + 1], acc);
                 acc = mma32(c0, c1, Sh[kg], Sh[kg + 1], acc);
             }
             if (NTK & 1) {
-                const bf16x4 a0 = lds4(mh + 16 * kg + 4 * g), c0 = lds4(ml + 16 * kg + 4 * g);
+                const bf16x4 a0 = lds4_tr(sMh, SM, 16 * kg, 16 * nt, g, c16);
+                const bf16x4 c0 = lds4_tr(sMl, SM, 16 * kg, 16 * nt, g, c16);
                 acc = mma16(a0, Sh[kg], acc);
                 acc = mma16(a0, Sl[kg], acc);
                 acc = mma16(c0, Sh[kg], acc);

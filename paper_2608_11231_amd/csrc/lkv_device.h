@@ -69,6 +69,21 @@ __device__ __forceinline__ Split4 split4(f32x4 x) {
 __device__ __forceinline__ bf16x4 lds4(const bf16* p) { return *reinterpret_cast<const bf16x4*>(p); }
 __device__ __forceinline__ f32x4 lds4f(const float* p) { return *reinterpret_cast<const f32x4*>(p); }
 
+// Transposed fragment read (gfx950 ds_read_b64_tr_b16).  Within each group of
+// 16 lanes the instruction takes the 16 four-element vectors the lanes address
+// as one 64-element run and hands lane i every 16th element starting at i.  With
+// lane i of group g addressing M[r0 + 4g + i/4][c0 + 4(i%4)] of a row-major
+// bf16 LDS matrix M, lane (g, c) receives M[r0 + 4g + j][c0 + c], j = 0..3:
+// the MFMA operand fragment of M^T (row c0 + c, contraction rows r0 + 4g + j)
+// without a transposed copy of M.
+typedef short lds_i16x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ bf16x4 lds4_tr(const bf16* M, int stride, int r0, int c0, int g, int c) {
+    const bf16* a = M + (r0 + 4 * g + (c >> 2)) * stride + c0 + 4 * (c & 3);
+    typedef __attribute__((address_space(3))) lds_i16x4 lds_ptr_t;
+    const lds_i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_ptr_t*)(a));
+    return __builtin_bit_cast(bf16x4, v);
+}
+
 // Inclusive prefix sum across the 64 lanes of a wave.
 __device__ __forceinline__ float wave_incl_scan(float x, int lane) {
 #pragma unroll
