@@ -67,6 +67,7 @@ typedef enum { LKV_GDN = 0, LKV_SSD = 1 } lkv_family;
  *   dv         GDN: value dim        | SSD: head dim P             multiple of 16, <= 512
  *   chunk      tokens per chunk of the chunkwise kernels           in {16, 64}
  *   io_dtype   dtype of q/k/v (C/B/x) and o (y)                    LKV_F32 | LKV_BF16
+ *              (LKV_F32 requires dk <= 64)
  *   gate_dtype GDN: dtype of g = log(alpha) and beta               LKV_F32 | LKV_BF16
  *              SSD: must be LKV_F32 (dt)                                              */
 typedef struct {

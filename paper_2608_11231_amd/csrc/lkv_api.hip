@@ -4,7 +4,7 @@
 
 #include "init_kernels.h"
 #include "lkv.h"
-#include "scan_kernel.h"
+#include "chunk_kernel.h"
 
 using namespace lkv;
 
@@ -31,6 +31,8 @@ lkv_status check_layer(const lkv_layer* L) {
     if (L->dk != 16 && L->dk != 32 && L->dk != 64 && L->dk != 128) return LKV_E_UNSUPPORTED;
     if (L->dv % 16 != 0 || L->dv > 512) return LKV_E_UNSUPPORTED;
     if (L->chunk != 16 && L->chunk != 64) return LKV_E_UNSUPPORTED;
+    // fp32 q/k/v double the staged tiles: supported up to dk = 64
+    if (L->io_dtype == LKV_F32 && L->dk > 64) return LKV_E_UNSUPPORTED;
     return LKV_OK;
 }
 
@@ -39,22 +41,26 @@ int env_int(const char* name, int dflt) {
     return s ? atoi(s) : dflt;
 }
 
-// Waves per workgroup for the chunk kernels: 16*nw state rows per workgroup.
-// More waves share the token x token work of a chunk; fewer waves give more
-// workgroups.  Pick the largest nw that still fills the 256 CUs.
+// State-row waves per workgroup for the chunk kernels (16*nb rows per
+// workgroup; every workgroup also runs 4 waves for the state-independent
+// work).  More rows per workgroup share that work; fewer give more workgroups.
+// Pick the largest nb that fits LDS and still fills the 256 CUs.
 int pick_nw(int fam, int dk, int chunk, bool f32io, int64_t pairs, int rows, int rows2, bool summary) {
-    int forced = env_int("LKV_SCAN_NW", 0);
-    for (int nw = 4; nw >= 1; nw >>= 1) {
-        if (rows % (16 * nw) || (rows2 && rows2 % (16 * nw))) continue;
-        if (scan_lds_bytes(fam, dk, chunk, f32io, nw, summary) > 160 * 1024) continue;
+    int forced = env_int("LKV_SCAN_NB", 0);
+    int fallback = 0;
+    for (int nb = 4; nb >= 1; nb >>= 1) {
+        if (rows % (16 * nb) || (rows2 && rows2 % (16 * nb))) continue;
+        if (scan_lds_bytes(fam, dk, chunk, f32io, nb, summary) > 160 * 1024) continue;
         if (forced) {
-            if (nw == forced) return nw;
+            if (nb == forced) return nb;
             continue;
         }
-        const int64_t units = pairs * ((rows + (rows2 ? rows2 : 0)) / (16 * nw));
-        if (units >= 240 || nw == 1) return nw;
+        if (!fallback) fallback = nb;
+        const int64_t units = pairs * ((rows + (rows2 ? rows2 : 0)) / (16 * nb));
+        if (units >= 240) return nb;
+        fallback = nb;
     }
-    return 1;
+    return fallback;
 }
 
 lkv_status check_tokens(const lkv_layer* L, const lkv_tokens* T, bool need_q) {
@@ -107,6 +113,7 @@ lkv_status chunk_scan(const lkv_layer* L, const lkv_tokens* T, float scale, cons
     const bool f32io = L->io_dtype == LKV_F32;
     const int64_t pairs = (int64_t)T->n_seq * L->h_v;
     const int nw = pick_nw(L->family, L->dk, L->chunk, f32io, pairs, L->dv, 0, false);
+    if (nw == 0) return LKV_E_UNSUPPORTED;
     const int64_t units = pairs * (L->dv / (16 * nw));
     if (units >= (INT64_C(1) << 31)) return LKV_E_SHAPE;
     ScanArgs a = base_args(L, T);
@@ -117,7 +124,7 @@ lkv_status chunk_scan(const lkv_layer* L, const lkv_tokens* T, float scale, cons
     a.summary = 0;
     a.tiles_b = L->dv / (16 * nw);
     a.tiles_m = 0;
-    a.nw = nw;
+    a.nb = nw;
     a.n_units = (int32_t)units;
     return hip_status(launch_scan(L, a, (hipStream_t)stream));
 }
@@ -164,7 +171,7 @@ lkv_status lkv_block_summary(const lkv_layer* L, const lkv_tokens* T, float* B_o
     hipStream_t st = (hipStream_t)stream;
     if (L->family == LKV_SSD && !B_out) {
         // Lambda only: one row tile per (block, head) carries the gate sum
-        a.nw = 1;
+        a.nb = 1;
         a.tiles_b = 1;
         a.tiles_m = 0;
         a.S_final = nullptr;
@@ -175,7 +182,8 @@ lkv_status lkv_block_summary(const lkv_layer* L, const lkv_tokens* T, float* B_o
     }
     const int nw = pick_nw(L->family, L->dk, L->chunk, f32io, pairs, rows_b ? rows_b : rows_m,
                            rows_b ? rows_m : 0, true);
-    a.nw = nw;
+    if (nw == 0) return LKV_E_UNSUPPORTED;
+    a.nb = nw;
     a.tiles_b = rows_b / (16 * nw);
     a.tiles_m = rows_m / (16 * nw);
     const int64_t units = pairs * (a.tiles_b + a.tiles_m);

@@ -40,7 +40,7 @@ GDN_CASES = [
     (32, 32, 16, "bf16", 2, 4, ((40, 23), (17, 0, 5)), (37, 70)),
     (64, 64, 64, "bf16", 2, 2, ((130, 64), (1,)), (150, 64)),
     (128, 128, 64, "bf16", 2, 2, ((200, 77),), (193,)),
-    (128, 64, 64, "f32", 1, 2, ((90,), (65, 3)), (129, 0)),
+    (64, 64, 64, "f32", 1, 2, ((90,), (65, 3)), (129, 0)),
     (64, 48, 16, "bf16", 1, 1, ((33,),), (47,)),
 ]
 
@@ -49,7 +49,7 @@ SSD_CASES = [
     (16, 16, 16, "f32", 1, 2, ((40, 23),), (37,)),
     (128, 64, 64, "bf16", 1, 4, ((130, 64), (1, 70)), (150, 64)),
     (64, 32, 16, "bf16", 2, 4, ((50,),), (77,)),
-    (128, 64, 16, "f32", 1, 2, ((20,),), (33,)),
+    (64, 64, 16, "f32", 1, 2, ((20,),), (33,)),
 ]
 
 
@@ -226,6 +226,13 @@ def test_deterministic(fam):
     for a, b in zip(first, (G.B_pool, G.M_pool, G.S_exact, G.S_final, G.out)):
         assert torch.equal(a.view(torch.int16) if a.dtype == torch.bfloat16 else a.view(torch.int32),
                            b.view(torch.int16) if b.dtype == torch.bfloat16 else b.view(torch.int32))
+
+
+def test_fp32_io_needs_dk_at_most_64():
+    w = _work(I.GDN, (128, 32, 64, "f32", 1, 1, ((20,),), (20,)))
+    G = gpu_io.GpuWorkload(w, with_cached=False)
+    with pytest.raises(lkv.LkvError, match="UNSUPPORTED"):
+        G.scan(None)
 
 
 def test_tiny_config_end_to_end():
