@@ -244,6 +244,20 @@ def main():
     T = w.online.n_tok
     work = work_model(w)
     roofs = {name: roofline(name, work[name], per_op[name]) for name in per_op}
+    # measured HBM traffic per launch, from the committed rocprofv3 counter summary of
+    # this workload -- only when it was taken on the current kernel sources
+    from paper_2608_11231_amd import rocprof_summary
+    table = rocprof_summary.read_traffic(os.path.join(ROOT, "profiles", f"{w.name}_hbm_traffic.txt"))
+    if table:
+        fam = w.layer.family
+        pick = {"scan": lambda n: n.startswith(f"lkv::chunk_kernel<{fam},") and n.endswith(",false>"),
+                "fold": lambda n: n.startswith(f"lkv::chunk_kernel<{fam},") and n.endswith(",true>"),
+                "compose": lambda n: "compose" in n,
+                "init_single": lambda n: "init_single" in n}
+        for op, pred in pick.items():
+            cand = [v for (n, grid), v in table.items() if pred(n)]
+            if len(cand) == 1:
+                roofs[op]["traffic"] = round(cand[0])
     dominant = max(per_op, key=per_op.get)
     L = w.layer
     result = {
