@@ -17,8 +17,11 @@ hipError_t launch_scan_ssd(int dk, int chunk, bool f32io, const ScanArgs& a, hip
 
 size_t scan_lds_bytes(int fam, int dk, int chunk, bool f32io, int nb, bool summary) {
 #define LKV_LDS(FAM_, DK_, CH_)                                                              \
-    if (dk == DK_ && chunk == CH_)                                                           \
-        return f32io ? chunk_lds_t<FAM_, DK_, CH_, true>(nb, summary) : chunk_lds_t<FAM_, DK_, CH_, false>(nb, summary);
+    if (dk == DK_ && chunk == CH_) {                                                         \
+        if (!f32io) return chunk_lds_t<FAM_, DK_, CH_, false>(nb, summary);                   \
+        if constexpr (DK_ <= 64) return chunk_lds_t<FAM_, DK_, CH_, true>(nb, summary);       \
+        return 0;                                                                            \
+    }
     if (fam == FAM_GDN) {
         LKV_LDS(FAM_GDN, 16, 16) LKV_LDS(FAM_GDN, 32, 16) LKV_LDS(FAM_GDN, 64, 16) LKV_LDS(FAM_GDN, 128, 16)
         LKV_LDS(FAM_GDN, 16, 64) LKV_LDS(FAM_GDN, 32, 64) LKV_LDS(FAM_GDN, 64, 64) LKV_LDS(FAM_GDN, 128, 64)

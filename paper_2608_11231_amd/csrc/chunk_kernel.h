@@ -184,20 +184,25 @@ __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
                 }
 #pragma unroll
                 for (int mt = 0; mt < NTC; ++mt) {
-                    f32x4 vv = zero4();
+                    X[mt] = zero4();
                     if (load_v) {
-                        vv = to_f32(lds4_tr(sV(b), SV, 16 * mt, 16 * w, g, c16));
-                        if (F32IO) vv += to_f32(lds4_tr(sV(b) + VPL, SV, 16 * mt, 16 * w, g, c16));
+                        X[mt] = to_f32(lds4_tr(sV(b), SV, 16 * mt, 16 * w, g, c16));
+                        if (F32IO) X[mt] += to_f32(lds4_tr(sV(b) + VPL, SV, 16 * mt, 16 * w, g, c16));
                     }
-                    if (FAM == FAM_GDN) {
-                        const f32x4 bt = lds4f(G + 2 * CH + 16 * mt + 4 * g);
-                        const bf16* kr = Kb + (16 * mt + c16) * SK;
-                        const f32x4 ks = gemm_lds_reg<F32IO, true>(kr, kr + KPL, Sh, Sl, 0, NTK, g, zero4());
-                        const f32x4 be = lds4f(G + CH + 16 * mt + 4 * g);
+                }
+                if (FAM == FAM_GDN) {
+                    // K S^T for all token tiles at once (interleaved chains, hi and lo passes apart)
+                    f32x4 kh[NTC], kl[NTC];
 #pragma unroll
-                        for (int r = 0; r < 4; ++r) X[mt][r] = be[r] * (vv[r] - bt[r] * ks[r]);
-                    } else {
-                        X[mt] = vv;
+                    for (int mt = 0; mt < NTC; ++mt) kh[mt] = kl[mt] = zero4();
+                    mgemm_rows<NTC, F32IO, true>(Kb + c16 * SK, 16 * SK, KPL, Sh, Sl, NTK, g, kh, kl);
+#pragma unroll
+                    for (int mt = 0; mt < NTC; ++mt) {
+                        const f32x4 bt = lds4f(G + 2 * CH + 16 * mt + 4 * g);
+                        const f32x4 be = lds4f(G + CH + 16 * mt + 4 * g);
+                        const f32x4 ks = kh[mt] + kl[mt];
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) X[mt][r] = be[r] * (X[mt][r] - bt[r] * ks[r]);
                     }
                 }
             }
@@ -209,17 +214,25 @@ __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
                 f32x4 U[NTC];
                 bf16x4 Uh[NTC], Ul[NTC];
                 if (FAM == FAM_GDN) {
-                    // U_mt = N_mt (beta X_mt - sum_{m<mt} L_{mt,m} U_m)   (blocks of 16 tokens)
+                    // U_mt = N_mt (beta X_mt - sum_{m<mt} L_{mt,m} U_m)   (blocks of 16 tokens);
+                    // the hi*hi and the correction passes accumulate apart
                     const bf16* LT = sLT(b);
                     const bf16* NT = sNT(b);
 #pragma unroll
                     for (int mt = 0; mt < NTC; ++mt) {
-                        const f32x4 acc = gemm_blk_reg<SB, true, true>(
-                            [&](int kg) { return LT + off_index(mt, kg) * BLK; }, NOFF * BLK, Uh, Ul, 0, mt, g, c16,
-                            X[mt]);
-                        const Split4 rs = split4(acc);
-                        U[mt] = gemm_blk_reg<SB, true, true>([&](int) { return NT + mt * BLK; }, NTC * BLK, &rs.hi,
-                                                             &rs.lo, 0, 1, g, c16, zero4());
+                        auto lhi = [&](int kg) { return LT + off_index(mt, kg) * BLK; };
+                        auto llo = [&](int kg) { return LT + NOFF * BLK + off_index(mt, kg) * BLK; };
+                        // hi*hi onto X; hi*lo and lo*hi in a second accumulator
+                        const f32x4 a0 = gemm_blk_reg<SB, false, false>(lhi, 0, Uh, Uh, 0, mt, g, c16, X[mt]);
+                        f32x4 a1 = gemm_blk_reg<SB, false, false>(lhi, 0, Ul, Ul, 0, mt, g, c16, zero4());
+                        a1 = gemm_blk_reg<SB, false, false>(llo, 0, Uh, Uh, 0, mt, g, c16, a1);
+                        const Split4 rs = split4(a0 + a1);
+                        const bf16* nb = NT + mt * BLK;
+                        const bf16x4 nh = lds4_tr(nb, SB, 0, 0, g, c16), nl = lds4_tr(nb + NTC * BLK, SB, 0, 0, g, c16);
+                        f32x4 u0 = mma16(nh, rs.hi, zero4());
+                        f32x4 u1 = mma16(nh, rs.lo, zero4());
+                        u1 = mma16(nl, rs.hi, u1);
+                        U[mt] = u0 + u1;
                         const Split4 us = split4(U[mt]);
                         Uh[mt] = us.hi;
                         Ul[mt] = us.lo;
@@ -240,29 +253,64 @@ __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
                         for (int nt = 0; nt < NTK; ++nt) Sl[nt] = to_bf16(S[nt] - to_f32(Sh[nt]));
                     }
                     const float coef = (FAM == FAM_GDN) ? p.scale : 1.f;
+                    // Q S^T for all token tiles (interleaved), then the masked P U term
+                    f32x4 qh[NTC], ql[NTC];
+#pragma unroll
+                    for (int mt = 0; mt < NTC; ++mt) qh[mt] = ql[mt] = zero4();
+                    mgemm_rows<NTC, F32IO, F32IO>(sQ(b) + c16 * SK, 16 * SK, KPL, Sh, Sl, NTK, g, qh, ql);
+                    f32x4 O[NTC];
 #pragma unroll
                     for (int mt = 0; mt < NTC; ++mt) {
-                        const bf16* qr = sQ(b) + (16 * mt + c16) * SK;
-                        const f32x4 qs = F32IO ? gemm_lds_reg<true, true>(qr, qr + KPL, Sh, Sl, 0, NTK, g, zero4())
-                                               : gemm_lds_reg<false, false>(qr, qr, Sh, Sh, 0, NTK, g, zero4());
                         const f32x4 bt = lds4f(G + 2 * CH + 16 * mt + 4 * g);
-                        f32x4 o;
+                        const f32x4 qs = F32IO ? qh[mt] + ql[mt] : qh[mt];
 #pragma unroll
-                        for (int r = 0; r < 4; ++r) o[r] = coef * bt[r] * qs[r];
-                        o = gemm_blk_reg<SB, F32IO, F32IO>([&](int kg) { return PT + low_index(mt, kg) * BLK; },
-                                                           NPB * BLK, Uh, Ul, 0, mt + 1, g, c16, o);
+                        for (int r = 0; r < 4; ++r) O[mt][r] = coef * bt[r] * qs[r];
+                    }
+                    // P U: tile mt contracts over token blocks 0..mt; pair index outer, tiles inner
+                    if (NTC == 1) {
+                        const bf16x4 x = lds4_tr(PT, SB, 0, 0, g, c16);
+                        O[0] = mma16(x, Uh[0], O[0]);
+                        if (F32IO) {
+                            O[0] = mma16(x, Ul[0], O[0]);
+                            O[0] = mma16(lds4_tr(PT + NPB * BLK, SB, 0, 0, g, c16), Uh[0], O[0]);
+                        }
+                    } else {
+#pragma unroll
+                        for (int kp = 0; kp < NTC; kp += 2) {
+#pragma unroll
+                            for (int mt = 0; mt < NTC; ++mt) {
+                                if (mt < kp) continue;
+                                const bool two = mt >= kp + 1;
+                                const bf16* x0p = PT + low_index(mt, kp) * BLK;
+                                const bf16x4 x0 = lds4_tr(x0p, SB, 0, 0, g, c16);
+                                const bf16x4 x1 = two ? lds4_tr(x0p + BLK, SB, 0, 0, g, c16) : zero_bf16x4();
+                                const bf16x4 u1h = two ? Uh[kp + 1] : zero_bf16x4();
+                                O[mt] = mma32(x0, x1, Uh[kp], u1h, O[mt]);
+                                if (F32IO) {
+                                    const bf16x4 u1l = two ? Ul[kp + 1] : zero_bf16x4();
+                                    O[mt] = mma32(x0, x1, Ul[kp], u1l, O[mt]);
+                                    const bf16x4 y0 = lds4_tr(x0p + NPB * BLK, SB, 0, 0, g, c16);
+                                    const bf16x4 y1 = two ? lds4_tr(x0p + NPB * BLK + BLK, SB, 0, 0, g, c16)
+                                                          : zero_bf16x4();
+                                    O[mt] = mma32(y0, y1, Uh[kp], u1h, O[mt]);
+                                }
+                            }
+                        }
+                    }
+#pragma unroll
+                    for (int mt = 0; mt < NTC; ++mt) {
 #pragma unroll
                         for (int r = 0; r < 4; ++r) {
                             const int t = 16 * mt + 4 * g + r;
                             if (t < n) {
                                 const int64_t oi = ((c0 + t) * p.h_v + h) * (int64_t)p.dv + my_row;
-                                if (F32IO) reinterpret_cast<float*>(p.out)[oi] = o[r];
-                                else reinterpret_cast<bf16*>(p.out)[oi] = (bf16)o[r];
+                                if (F32IO) reinterpret_cast<float*>(p.out)[oi] = O[mt][r];
+                                else reinterpret_cast<bf16*>(p.out)[oi] = (bf16)O[mt][r];
                             }
                         }
                     }
                 }
-                // S <- b_C S + K^T diag(w) U
+                // S <- b_C S + K^T diag(w) U   (all dk tiles interleaved)
                 bf16x4 Wh[NTC], Wl[NTC];
 #pragma unroll
                 for (int mt = 0; mt < NTC; ++mt) {
@@ -273,8 +321,8 @@ __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
                 }
                 const float bC = G[4 * CH];
 #pragma unroll
-                for (int nt = 0; nt < NTK; ++nt)
-                    S[nt] = gemm_ldstr_reg<F32IO, true>(Kb, Kb + KPL, SK, 16 * nt, Wh, Wl, 0, NTC, g, c16, bC * S[nt]);
+                for (int nt = 0; nt < NTK; ++nt) S[nt] = bC * S[nt];
+                mgemm_tr<NTK, F32IO, true>(Kb, KPL, SK, Wh, Wl, NTC, g, c16, S);
             }
         }
         float* dst = mtile ? p.M_out : p.S_final;
@@ -375,6 +423,13 @@ __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
                 // finished entry goes straight to NT[c16][m] = N[m][c16] (bf16 hi / lo)
                 bf16* nt_hi = sNT(b) + mt * BLK + c16 * SB;
                 bf16* nt_lo = nt_hi + NTC * BLK;
+                // the whole block in registers first (columns of L are rows of LTd), so the
+                // 16 dependent steps below wait on FMAs only, not on LDS
+                f32x4 Lc[15][4];
+#pragma unroll
+                for (int m = 0; m < 15; ++m)
+#pragma unroll
+                    for (int q4 = (m + 1) >> 2; q4 < 4; ++q4) Lc[m][q4] = lds4f(LTd + m * SLD + 4 * q4);
                 float a[16];
 #pragma unroll
                 for (int i = 0; i < 16; ++i) a[i] = 0.f;
@@ -387,14 +442,8 @@ __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
                         nt_lo[m] = (bf16)(xm - (float)hi);
                     }
                     if (m < 15) {
-                        const float* col = LTd + m * SLD;  // column m of L
 #pragma unroll
-                        for (int i4 = (m + 1) & ~3; i4 < 16; i4 += 4) {
-                            const f32x4 cv = lds4f(col + i4);
-#pragma unroll
-                            for (int e = 0; e < 4; ++e)
-                                if (i4 + e > m) a[i4 + e] += cv[e] * xm;
-                        }
+                        for (int i = m + 1; i < 16; ++i) a[i] += Lc[m][i >> 2][i & 3] * xm;
                     }
                 }
             }

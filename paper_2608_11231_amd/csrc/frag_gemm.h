@@ -111,40 +111,105 @@ __device__ __forceinline__ f32x4 gemm_blk_reg(BlkFn blk, int plane, const bf16x4
     return acc;
 }
 
+// Multi-tile products with interleaved accumulation chains.  One MFMA chain
+// per output tile serialises on the matrix-core latency; looping over the
+// contraction slices outside and the tiles inside keeps NM independent chains
+// in flight.  nk = number of 16-slices (1, or even).
+
+// acc_h[m] += A_m x B (hi passes), acc_l[m] += lo passes, for NM tiles whose A
+// rows are LDS rows `a0 + m * mstep` (this lane's row, hi plane; lo plane at
+// + plane), B = acc-layout register tiles.
+template <int NM, bool ALO, bool BLO>
+__device__ __forceinline__ void mgemm_rows(const bf16* a0, int mstep, int plane, const bf16x4* bh,
+                                           const bf16x4* bl, int nk, int g, f32x4* acc_h, f32x4* acc_l) {
+    if (nk == 1) {
+#pragma unroll
+        for (int m = 0; m < NM; ++m) {
+            const bf16* ar = a0 + m * mstep + 4 * g;
+            const bf16x4 x = lds4(ar);
+            acc_h[m] = mma16(x, bh[0], acc_h[m]);
+            if (BLO) acc_l[m] = mma16(x, bl[0], acc_l[m]);
+            if (ALO) acc_l[m] = mma16(lds4(ar + plane), bh[0], acc_l[m]);
+        }
+        return;
+    }
+#pragma unroll
+    for (int kg = 0; kg < 8; kg += 2) {
+        if (kg >= nk) break;
+#pragma unroll
+        for (int m = 0; m < NM; ++m) {
+            const bf16* ar = a0 + m * mstep + 16 * kg + 4 * g;
+            const bf16x4 x0 = lds4(ar), x1 = lds4(ar + 16);
+            acc_h[m] = mma32(x0, x1, bh[kg], bh[kg + 1], acc_h[m]);
+            if (BLO) acc_l[m] = mma32(x0, x1, bl[kg], bl[kg + 1], acc_l[m]);
+            if (ALO) acc_l[m] = mma32(lds4(ar + plane), lds4(ar + plane + 16), bh[kg], bh[kg + 1], acc_l[m]);
+        }
+    }
+}
+
+// acc[n] += M^T(columns 16n..16n+15) x B for NN tiles, the A fragments read
+// transposed from a row-major LDS matrix M (rows = contraction, hi plane; lo
+// plane at + plane).  All passes accumulate into acc[n].
+template <int NN, bool ALO, bool BLO>
+__device__ __forceinline__ void mgemm_tr(const bf16* M, int plane, int stride, const bf16x4* bh, const bf16x4* bl,
+                                         int nk, int g, int c, f32x4* acc) {
+    if (nk == 1) {
+#pragma unroll
+        for (int n = 0; n < NN; ++n) {
+            const bf16x4 x = lds4_tr(M, stride, 0, 16 * n, g, c);
+            acc[n] = mma16(x, bh[0], acc[n]);
+            if (BLO) acc[n] = mma16(x, bl[0], acc[n]);
+            if (ALO) acc[n] = mma16(lds4_tr(M + plane, stride, 0, 16 * n, g, c), bh[0], acc[n]);
+        }
+        return;
+    }
+#pragma unroll
+    for (int kg = 0; kg < 8; kg += 2) {
+        if (kg >= nk) break;
+#pragma unroll
+        for (int n = 0; n < NN; ++n) {
+            const bf16x4 x0 = lds4_tr(M, stride, 16 * kg, 16 * n, g, c);
+            const bf16x4 x1 = lds4_tr(M, stride, 16 * kg + 16, 16 * n, g, c);
+            acc[n] = mma32(x0, x1, bh[kg], bh[kg + 1], acc[n]);
+            if (BLO) acc[n] = mma32(x0, x1, bl[kg], bl[kg + 1], acc[n]);
+            if (ALO) {
+                const bf16x4 y0 = lds4_tr(M + plane, stride, 16 * kg, 16 * n, g, c);
+                const bf16x4 y1 = lds4_tr(M + plane, stride, 16 * kg + 16, 16 * n, g, c);
+                acc[n] = mma32(y0, y1, bh[kg], bh[kg + 1], acc[n]);
+            }
+        }
+    }
+}
+
 // acc += A(LDS rows) x B(LDS rows)^T over DK, both read with the same pattern.
 template <int DK, bool LO>
 __device__ __forceinline__ f32x4 gemm_lds_lds(const bf16* ah, const bf16* al_, const bf16* bh, const bf16* bl,
                                               int g, f32x4 acc) {
     constexpr int NK = DK / 16;
+    if (NK == 1) {
+        const int o0 = 4 * g;
+        const bf16x4 a0 = lds4(ah + o0), b0 = lds4(bh + o0);
+        acc = mma16(a0, b0, acc);
+        if (LO) {
+            acc = mma16(a0, lds4(bl + o0), acc);
+            acc = mma16(lds4(al_ + o0), b0, acc);
+        }
+        return acc;
+    }
+    // even and odd slice pairs accumulate separately: two chains in flight
+    f32x4 acc2 = zero4();
 #pragma unroll
     for (int kg = 0; kg + 1 < NK; kg += 2) {
         const int o0 = 16 * kg + 4 * g, o1 = o0 + 16;
         const bf16x4 a0 = lds4(ah + o0), a1 = lds4(ah + o1), b0 = lds4(bh + o0), b1 = lds4(bh + o1);
-        acc = mma32(a0, a1, b0, b1, acc);
+        f32x4& t = ((kg >> 1) & 1) ? acc2 : acc;
+        t = mma32(a0, a1, b0, b1, t);
         if (LO) {
-            acc = mma32(a0, a1, lds4(bl + o0), lds4(bl + o1), acc);
-            acc = mma32(lds4(al_ + o0), lds4(al_ + o1), b0, b1, acc);
+            t = mma32(a0, a1, lds4(bl + o0), lds4(bl + o1), t);
+            t = mma32(lds4(al_ + o0), lds4(al_ + o1), b0, b1, t);
         }
     }
-    if (NK & 1) {
-        const int o0 = 16 * (NK - 1) + 4 * g;
-        const bf16x4 a0 = lds4(ah + o0), b0 = lds4(bh + o0);
-        if (NK == 1) {
-            acc = mma16(a0, b0, acc);
-            if (LO) {
-                acc = mma16(a0, lds4(bl + o0), acc);
-                acc = mma16(lds4(al_ + o0), b0, acc);
-            }
-        } else {
-            const bf16x4 z = zero_bf16x4();
-            acc = mma32(a0, z, b0, z, acc);
-            if (LO) {
-                acc = mma32(a0, z, lds4(bl + o0), z, acc);
-                acc = mma32(lds4(al_ + o0), z, b0, z, acc);
-            }
-        }
-    }
-    return acc;
+    return acc + acc2;
 }
 
 // Store an acc tile (rows 4g+r, column c) TRANSPOSED into a 16x16 block:
