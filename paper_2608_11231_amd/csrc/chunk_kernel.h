@@ -36,6 +36,8 @@
 // feed the bf16 output use the hi part.  With fp32 inputs every operand is
 // split.
 #pragma once
+#include <type_traits>
+
 #include "frag_gemm.h"
 
 namespace lkv {
@@ -72,7 +74,10 @@ struct ChunkLds {
     static constexpr int NTC = CH / 16;
     static constexpr int NOFF = NTC * (NTC - 1) / 2;  // strictly-lower 16x16 blocks
     static constexpr int NPB = NTC * (NTC + 1) / 2;   // lower blocks incl. the diagonal
-    static constexpr int SK = DK + 8;                 // bf16 stride of [tok][dk] rows
+    // bf16 stride of [tok][dk] rows (kq_pos order): 16-byte aligned rows whose
+    // fragment reads (16-byte row runs and transposed 8-byte reads) are free of
+    // LDS bank conflicts
+    static constexpr int SK = DK >= 32 ? DK + 16 : DK + 8;
     static constexpr int SV = 16 * NB + 8;            // bf16 stride of [tok][rows] rows
     static constexpr int SB = 20;                     // bf16 stride of a 16x16 block
     static constexpr int BLK = 16 * SB;               // elements per block plane
@@ -84,7 +89,8 @@ struct ChunkLds {
     static constexpr size_t K_SZ = al(size_t(PL) * CH * SK * 2);
     static constexpr size_t Q_SZ = HAS_Q ? al(size_t(PL) * CH * SK * 2) : 0;
     static constexpr size_t V_SZ = al(size_t(PL) * CH * SV * 2);
-    static constexpr size_t G_SZ = al((4 * CH + 4) * 4);
+    // gate rows: raw gate | beta | b | w | cumulative gate gc | b_C, gc_C
+    static constexpr size_t G_SZ = al((5 * CH + 4) * 4);
     static constexpr size_t LT_SZ = HAS_L ? al(size_t(NOFF) * BLK * 2 * 2) : 0;
     static constexpr size_t NT_SZ = HAS_L ? al(size_t(NTC) * BLK * 2 * 2) : 0;
     static constexpr size_t PT_SZ = HAS_Q ? al(size_t(NPB) * BLK * PL * 2) : 0;
@@ -98,12 +104,24 @@ struct ChunkLds {
     static constexpr size_t BUF = PT_OFF + PT_SZ;  // one pipeline buffer
     static constexpr size_t GC_OFF = 2 * BUF;      // per A-wave gate prefix
     static constexpr size_t INV_OFF = GC_OFF + al(NA * 64 * 4);
-    static constexpr size_t BYTES = INV_OFF + (HAS_L ? al(size_t(NA) * 16 * SLD * 4) : 0);
+    static constexpr int INV_BST = 16 * SLD + 4;      // f32 stride of inverse scratch blocks (bank shift)
+    static constexpr size_t BYTES = INV_OFF + (HAS_L ? al(size_t(NTC) * INV_BST * 4) : 0);
 };
 
 // index of block (mt, nt) among the strictly-lower blocks (nt < mt) / lower blocks (nt <= mt)
 __device__ __forceinline__ constexpr int off_index(int mt, int nt) { return mt * (mt - 1) / 2 + nt; }
 __device__ __forceinline__ constexpr int low_index(int mt, int nt) { return mt * (mt + 1) / 2 + nt; }
+// row block of the j-th strictly-lower / lower block in that order
+__device__ __forceinline__ constexpr int off_mt(int j) {
+    int mt = 1;
+    while (off_index(mt + 1, 0) <= j) ++mt;
+    return mt;
+}
+__device__ __forceinline__ constexpr int low_mt(int j) {
+    int mt = 0;
+    while (low_index(mt + 1, 0) <= j) ++mt;
+    return mt;
+}
 
 template <int FAM, int DK, int CH, bool F32IO, int NB, bool SUMMARY>
 __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
@@ -135,7 +153,7 @@ __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
     t1 = t1 < t0 ? t0 : (t1 > p.n_tok ? p.n_tok : t1);
     const int nch = (int)((t1 - t0 + CH - 1) / CH);
     const bool with_out = !SUMMARY && p.out != nullptr;
-    const bool load_v = !mtile;
+    const bool load_v = SUMMARY ? !mtile : true;  // transition (M) tiles of a block summary skip V
     const float Ah = (FAM == FAM_SSD) ? p.A[h] : 0.f;
 
     auto sK = [&](int b) { return reinterpret_cast<bf16*>(smem + b * Ly::BUF + Ly::K_OFF); };
@@ -145,6 +163,102 @@ __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
     auto sLT = [&](int b) { return reinterpret_cast<bf16*>(smem + b * Ly::BUF + Ly::LT_OFF); };
     auto sNT = [&](int b) { return reinterpret_cast<bf16*>(smem + b * Ly::BUF + Ly::NT_OFF); };
     auto sPT = [&](int b) { return reinterpret_cast<bf16*>(smem + b * Ly::BUF + Ly::PT_OFF); };
+
+    // ---- state-independent token blocks of one chunk (buffer b).  Items are the
+    // 16x16 blocks: the strictly-lower K K^T blocks of Gated DeltaNet (kind L,
+    // stored negated as -L, hi / lo) and the lower Q K^T / C B^T output blocks
+    // (kind P).  A wave takes items SLOT, SLOT + NSLOT, ... of one kind, fixed at
+    // compile time, so all of its products run as independent accumulation
+    // chains.  gcp: the chunk's cumulative log-gates.
+    constexpr int NK = DK / 16;
+    auto items = [&](auto slot_c, auto nslot_c, auto kind_l_c, int b, const float* gcp) {
+        constexpr int SLOT = decltype(slot_c)::value;
+        constexpr int NSLOT = decltype(nslot_c)::value;
+        constexpr bool KL = decltype(kind_l_c)::value;
+        constexpr int NIT = KL ? (FAM == FAM_GDN ? NOFF : 0) : (SUMMARY ? 0 : NPB);
+        constexpr int NMY = NIT > SLOT ? (NIT - SLOT + NSLOT - 1) / NSLOT : 0;
+        if constexpr (NMY > 0) {
+            const bf16* Kb = sK(b);
+            const bf16* Ab = KL ? sK(b) : sQ(b);
+            const float* G = sG(b);
+            auto item_mt = [](int i) { return KL ? off_mt(SLOT + i * NSLOT) : low_mt(SLOT + i * NSLOT); };
+            auto item_nt = [](int i) {
+                const int j = SLOT + i * NSLOT;
+                return KL ? j - off_index(off_mt(j), 0) : j - low_index(low_mt(j), 0);
+            };
+            f32x4 acc[NMY];
+#pragma unroll
+            for (int i = 0; i < NMY; ++i) acc[i] = zero4();
+            if constexpr (NK == 1) {
+#pragma unroll
+                for (int i = 0; i < NMY; ++i) {
+                    const bf16* ar = Ab + (16 * item_mt(i) + c16) * SK + 4 * g;
+                    const bf16* br = Kb + (16 * item_nt(i) + c16) * SK + 4 * g;
+                    acc[i] = mma16(lds4(ar), lds4(br), acc[i]);
+                    if (F32IO) {
+                        acc[i] = mma16(lds4(ar), lds4(br + KPL), acc[i]);
+                        acc[i] = mma16(lds4(ar + KPL), lds4(br), acc[i]);
+                    }
+                }
+            } else {
+                // fragments of slice kp+1 are requested before the products of slice kp
+                constexpr int NKP = NK / 2, FPL = F32IO ? 2 : 1;
+                bf16x8 fa[2][FPL][NMY], fb[2][FPL][NMY];
+                auto fetch = [&](int kp, int buf) {
+#pragma unroll
+                    for (int i = 0; i < NMY; ++i) {
+                        const bf16* ar = Ab + (16 * item_mt(i) + c16) * SK + 32 * kp + 8 * g;
+                        const bf16* br = Kb + (16 * item_nt(i) + c16) * SK + 32 * kp + 8 * g;
+#pragma unroll
+                        for (int pl = 0; pl < FPL; ++pl) {
+                            fa[buf][pl][i] = lds8(ar + pl * KPL);
+                            fb[buf][pl][i] = lds8(br + pl * KPL);
+                        }
+                    }
+                };
+                fetch(0, 0);
+#pragma unroll
+                for (int kp = 0; kp < NKP; ++kp) {
+                    const int cb = kp & 1;
+                    if (kp + 1 < NKP) fetch(kp + 1, cb ^ 1);
+                    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                    for (int i = 0; i < NMY; ++i) {
+                        acc[i] = mma32(fa[cb][0][i], fb[cb][0][i], acc[i]);
+                        if constexpr (F32IO) {
+                            acc[i] = mma32(fa[cb][0][i], fb[cb][FPL - 1][i], acc[i]);
+                            acc[i] = mma32(fa[cb][FPL - 1][i], fb[cb][0][i], acc[i]);
+                        }
+                    }
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < NMY; ++i) {
+                const int mt = item_mt(i), nt = item_nt(i);
+                const int ic = 16 * nt + c16;
+                const float gci = gcp[ic];
+                const f32x4 gt = lds4f(gcp + 16 * mt + 4 * g);
+                f32x4 v;
+                if constexpr (KL) {
+                    const f32x4 bt = lds4f(G + CH + 16 * mt + 4 * g);
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) v[r] = -bt[r] * __expf(gt[r] - gci) * acc[i][r];
+                    store_tile_tr<SB, true>(sLT(b) + off_index(mt, nt) * BLK, NOFF * BLK, v, g, c16);
+                } else {
+                    const float cf = (FAM == FAM_GDN) ? p.scale : G[ic];  // SSD: dt of column i
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const float e = cf * __expf(gt[r] - gci) * acc[i][r];
+                        v[r] = (mt > nt || c16 <= 4 * g + r) ? e : 0.f;
+                    }
+                    store_tile_tr<SB, F32IO>(sPT(b) + low_index(mt, nt) * BLK, NPB * BLK, v, g, c16);
+                }
+            }
+        }
+    };
+    using std::integral_constant;
+    using L_KIND = std::true_type;
+    using P_KIND = std::false_type;
 
     // The two roles run separate loops with the same sequence of workgroup
     // barriers (s_barrier counts arriving waves, whatever the code location), so
@@ -163,6 +277,17 @@ __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
                 for (int r = 0; r < 4; ++r) S[nt][r] = (mtile && my_row == 16 * nt + 4 * g + r) ? 1.f : 0.f;
             }
         }
+        // bf16 hi / lo parts of the state, refreshed after every state update
+        bf16x4 Sh[NTK], Sl[NTK];
+        auto split_state = [&]() {
+#pragma unroll
+            for (int nt = 0; nt < NTK; ++nt) {
+                const Split4 sp = split4(S[nt]);
+                Sh[nt] = sp.hi;
+                Sl[nt] = sp.lo;
+            }
+        };
+        split_state();
         __syncthreads();  // prologue: chunk 0 staged by the A-waves
         for (int ci = 0; ci < nch; ++ci) {
             const int b = ci & 1;
@@ -171,23 +296,26 @@ __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
             __syncthreads();
             // ================= phase I: K S^T and the delta-rule right-hand side
             f32x4 X[NTC];
-            bf16x4 Sh[NTK];
             {
                 const bf16* Kb = sK(b);
                 const float* G = sG(b);
-                bf16x4 Sl[NTK];
-#pragma unroll
-                for (int nt = 0; nt < NTK; ++nt) {
-                    const Split4 sp = split4(S[nt]);
-                    Sh[nt] = sp.hi;
-                    Sl[nt] = sp.lo;
-                }
 #pragma unroll
                 for (int mt = 0; mt < NTC; ++mt) {
                     X[mt] = zero4();
                     if (load_v) {
                         X[mt] = to_f32(lds4_tr(sV(b), SV, 16 * mt, 16 * w, g, c16));
                         if (F32IO) X[mt] += to_f32(lds4_tr(sV(b) + VPL, SV, 16 * mt, 16 * w, g, c16));
+                    }
+                }
+                if (with_out) {
+                    // this chunk's output blocks P, shared by the B-waves (read after the barrier)
+                    using NS = integral_constant<int, NB>;
+                    const float* gcp = G + 4 * CH;
+                    switch (w) {
+                        case 0: items(integral_constant<int, 0>(), NS(), P_KIND(), b, gcp); break;
+                        case 1: items(integral_constant<int, 1 % NB>(), NS(), P_KIND(), b, gcp); break;
+                        case 2: items(integral_constant<int, 2 % NB>(), NS(), P_KIND(), b, gcp); break;
+                        default: items(integral_constant<int, 3 % NB>(), NS(), P_KIND(), b, gcp); break;
                     }
                 }
                 if (FAM == FAM_GDN) {
@@ -211,24 +339,103 @@ __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
             {
                 const bf16* Kb = sK(b);
                 const float* G = sG(b);
+                // Outputs are formed transposed, O^T = S Q^T + U^T P^T: tile mt holds
+                // O[16mt + c16][this wave's rows 4g..4g+3], so each lane stores 4
+                // consecutive state rows of one token.  S Q^T does not depend on U and
+                // is issued first, alongside the substitution chain.
+                f32x4 OT[NTC];
+                if (with_out) {
+                    const bf16* Qb = sQ(b);
+#pragma unroll
+                    for (int mt = 0; mt < NTC; ++mt) OT[mt] = zero4();
+                    if constexpr (NTK == 1) {
+#pragma unroll
+                        for (int mt = 0; mt < NTC; ++mt) {
+                            const bf16* qr = Qb + (16 * mt + c16) * SK + 4 * g;
+                            OT[mt] = mma16(Sh[0], lds4(qr), OT[mt]);
+                            if (F32IO) {
+                                OT[mt] = mma16(Sl[0], lds4(qr), OT[mt]);
+                                OT[mt] = mma16(Sh[0], lds4(qr + KPL), OT[mt]);
+                            }
+                        }
+                    } else {
+                        constexpr int NKP = NTK / 2;
+                        bf16x8 qh[NKP][NTC], ql[F32IO ? NKP : 1][NTC];
+#pragma unroll
+                        for (int kp = 0; kp < NKP; ++kp)
+#pragma unroll
+                            for (int mt = 0; mt < NTC; ++mt) {
+                                const bf16* qr = Qb + (16 * mt + c16) * SK + 32 * kp + 8 * g;
+                                qh[kp][mt] = lds8(qr);
+                                if constexpr (F32IO) ql[kp][mt] = lds8(qr + KPL);
+                            }
+                        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                        for (int kp = 0; kp < NKP; ++kp)
+#pragma unroll
+                            for (int mt = 0; mt < NTC; ++mt) {
+                                OT[mt] = mma32(Sh[2 * kp], Sh[2 * kp + 1], qh[kp][mt], OT[mt]);
+                                if constexpr (F32IO) {
+                                    OT[mt] = mma32(Sl[2 * kp], Sl[2 * kp + 1], qh[kp][mt], OT[mt]);
+                                    OT[mt] = mma32(Sh[2 * kp], Sh[2 * kp + 1], ql[kp][mt], OT[mt]);
+                                }
+                            }
+                    }
+                }
                 f32x4 U[NTC];
                 bf16x4 Uh[NTC], Ul[NTC];
+                // output blocks P (transposed fragments), independent of U: requested early
+                constexpr int PPL = (!SUMMARY && F32IO) ? 2 : 1;
+                bf16x4 Pf[PPL][SUMMARY ? 1 : NPB];
+                if (with_out) {
+#pragma unroll
+                    for (int j = 0; j < NPB; ++j)
+#pragma unroll
+                        for (int pl = 0; pl < PPL; ++pl)
+                            Pf[pl][j] = lds4_tr(sPT(b) + pl * NPB * BLK + j * BLK, SB, 0, 0, g, c16);
+                }
                 if (FAM == FAM_GDN) {
                     // U_mt = N_mt (beta X_mt - sum_{m<mt} L_{mt,m} U_m)   (blocks of 16 tokens);
-                    // the hi*hi and the correction passes accumulate apart
+                    // the hi*hi and the correction passes accumulate apart.  All L and N
+                    // fragments are in registers before the dependent chain starts.
                     const bf16* LT = sLT(b);
                     const bf16* NT = sNT(b);
+                    bf16x4 Lh[NOFF > 0 ? NOFF : 1], Ll[NOFF > 0 ? NOFF : 1], Nh[NTC], Nl[NTC];
+#pragma unroll
+                    for (int j = 0; j < NOFF; ++j) {
+                        Lh[j] = lds4_tr(LT + j * BLK, SB, 0, 0, g, c16);
+                        Ll[j] = lds4_tr(LT + (NOFF + j) * BLK, SB, 0, 0, g, c16);
+                    }
 #pragma unroll
                     for (int mt = 0; mt < NTC; ++mt) {
-                        auto lhi = [&](int kg) { return LT + off_index(mt, kg) * BLK; };
-                        auto llo = [&](int kg) { return LT + NOFF * BLK + off_index(mt, kg) * BLK; };
-                        // hi*hi onto X; hi*lo and lo*hi in a second accumulator
-                        const f32x4 a0 = gemm_blk_reg<SB, false, false>(lhi, 0, Uh, Uh, 0, mt, g, c16, X[mt]);
-                        f32x4 a1 = gemm_blk_reg<SB, false, false>(lhi, 0, Ul, Ul, 0, mt, g, c16, zero4());
-                        a1 = gemm_blk_reg<SB, false, false>(llo, 0, Uh, Uh, 0, mt, g, c16, a1);
+                        Nh[mt] = lds4_tr(NT + mt * BLK, SB, 0, 0, g, c16);
+                        Nl[mt] = lds4_tr(NT + (NTC + mt) * BLK, SB, 0, 0, g, c16);
+                    }
+                    // sum over token blocks kg < mt of A_{mt,kg} B_kg: pairs through the
+                    // 32-wide MFMA, a lone block through the 16-wide one, an odd tail after
+                    // pairs zero-padded (one shape per chain)
+                    auto blk_sum = [&](const bf16x4* A, const bf16x4* B, int mt, f32x4 acc) {
+                        int kg = 0;
+#pragma unroll
+                        for (; kg + 1 < mt; kg += 2)
+                            acc = mma32(A[off_index(mt, kg)], A[off_index(mt, kg + 1)], B[kg], B[kg + 1], acc);
+                        if (kg < mt) {
+                            if (kg == 0) {
+                                acc = mma16(A[off_index(mt, kg)], B[kg], acc);
+                            } else {
+                                const bf16x4 z = zero_bf16x4();
+                                acc = mma32(A[off_index(mt, kg)], z, B[kg], z, acc);
+                            }
+                        }
+                        return acc;
+                    };
+#pragma unroll
+                    for (int mt = 0; mt < NTC; ++mt) {
+                        const f32x4 a0 = blk_sum(Lh, Uh, mt, X[mt]);
+                        f32x4 a1 = blk_sum(Lh, Ul, mt, zero4());
+                        a1 = blk_sum(Ll, Uh, mt, a1);
                         const Split4 rs = split4(a0 + a1);
-                        const bf16* nb = NT + mt * BLK;
-                        const bf16x4 nh = lds4_tr(nb, SB, 0, 0, g, c16), nl = lds4_tr(nb + NTC * BLK, SB, 0, 0, g, c16);
+                        const bf16x4 nh = Nh[mt], nl = Nl[mt];
                         f32x4 u0 = mma16(nh, rs.hi, zero4());
                         f32x4 u1 = mma16(nh, rs.lo, zero4());
                         u1 = mma16(nl, rs.hi, u1);
@@ -246,33 +453,16 @@ __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
                     }
                 }
                 if (with_out) {
-                    const bf16* PT = sPT(b);
-                    bf16x4 Sl[NTK];
-                    if (F32IO) {
-#pragma unroll
-                        for (int nt = 0; nt < NTK; ++nt) Sl[nt] = to_bf16(S[nt] - to_f32(Sh[nt]));
-                    }
                     const float coef = (FAM == FAM_GDN) ? p.scale : 1.f;
-                    // Q S^T for all token tiles (interleaved), then the masked P U term
-                    f32x4 qh[NTC], ql[NTC];
 #pragma unroll
-                    for (int mt = 0; mt < NTC; ++mt) qh[mt] = ql[mt] = zero4();
-                    mgemm_rows<NTC, F32IO, F32IO>(sQ(b) + c16 * SK, 16 * SK, KPL, Sh, Sl, NTK, g, qh, ql);
-                    f32x4 O[NTC];
-#pragma unroll
-                    for (int mt = 0; mt < NTC; ++mt) {
-                        const f32x4 bt = lds4f(G + 2 * CH + 16 * mt + 4 * g);
-                        const f32x4 qs = F32IO ? qh[mt] + ql[mt] : qh[mt];
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) O[mt][r] = coef * bt[r] * qs[r];
-                    }
-                    // P U: tile mt contracts over token blocks 0..mt; pair index outer, tiles inner
-                    if (NTC == 1) {
-                        const bf16x4 x = lds4_tr(PT, SB, 0, 0, g, c16);
-                        O[0] = mma16(x, Uh[0], O[0]);
+                    for (int mt = 0; mt < NTC; ++mt) OT[mt] *= coef * G[2 * CH + 16 * mt + c16];
+                    // + U^T P^T: tile mt contracts over token blocks 0..mt, pairs of blocks per MFMA
+                    if constexpr (NTC == 1) {
+                        const bf16x4 x = Pf[0][0];
+                        OT[0] = mma16(Uh[0], x, OT[0]);
                         if (F32IO) {
-                            O[0] = mma16(x, Ul[0], O[0]);
-                            O[0] = mma16(lds4_tr(PT + NPB * BLK, SB, 0, 0, g, c16), Uh[0], O[0]);
+                            OT[0] = mma16(Ul[0], x, OT[0]);
+                            OT[0] = mma16(Uh[0], Pf[PPL - 1][0], OT[0]);
                         }
                     } else {
 #pragma unroll
@@ -281,32 +471,30 @@ __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
                             for (int mt = 0; mt < NTC; ++mt) {
                                 if (mt < kp) continue;
                                 const bool two = mt >= kp + 1;
-                                const bf16* x0p = PT + low_index(mt, kp) * BLK;
-                                const bf16x4 x0 = lds4_tr(x0p, SB, 0, 0, g, c16);
-                                const bf16x4 x1 = two ? lds4_tr(x0p + BLK, SB, 0, 0, g, c16) : zero_bf16x4();
+                                const int j0 = low_index(mt, kp);
+                                const bf16x4 x0 = Pf[0][j0];
+                                const bf16x4 x1 = two ? Pf[0][j0 + 1] : zero_bf16x4();
                                 const bf16x4 u1h = two ? Uh[kp + 1] : zero_bf16x4();
-                                O[mt] = mma32(x0, x1, Uh[kp], u1h, O[mt]);
+                                OT[mt] = mma32(Uh[kp], u1h, x0, x1, OT[mt]);
                                 if (F32IO) {
                                     const bf16x4 u1l = two ? Ul[kp + 1] : zero_bf16x4();
-                                    O[mt] = mma32(x0, x1, Ul[kp], u1l, O[mt]);
-                                    const bf16x4 y0 = lds4_tr(x0p + NPB * BLK, SB, 0, 0, g, c16);
-                                    const bf16x4 y1 = two ? lds4_tr(x0p + NPB * BLK + BLK, SB, 0, 0, g, c16)
-                                                          : zero_bf16x4();
-                                    O[mt] = mma32(y0, y1, Uh[kp], u1h, O[mt]);
+                                    OT[mt] = mma32(Ul[kp], u1l, x0, x1, OT[mt]);
+                                    const bf16x4 y0 = Pf[PPL - 1][j0];
+                                    const bf16x4 y1 = two ? Pf[PPL - 1][j0 + 1] : zero_bf16x4();
+                                    OT[mt] = mma32(Uh[kp], u1h, y0, y1, OT[mt]);
                                 }
                             }
                         }
                     }
+                    // one 8-byte (bf16) / 16-byte (fp32) store per lane and token tile
+                    const int64_t rowcol = (int64_t)h * p.dv + row0 + 16 * w + 4 * g;
 #pragma unroll
                     for (int mt = 0; mt < NTC; ++mt) {
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) {
-                            const int t = 16 * mt + 4 * g + r;
-                            if (t < n) {
-                                const int64_t oi = ((c0 + t) * p.h_v + h) * (int64_t)p.dv + my_row;
-                                if (F32IO) reinterpret_cast<float*>(p.out)[oi] = O[mt][r];
-                                else reinterpret_cast<bf16*>(p.out)[oi] = (bf16)O[mt][r];
-                            }
+                        const int t = 16 * mt + c16;
+                        if (t < n) {
+                            const int64_t oi = (c0 + t) * p.h_v * (int64_t)p.dv + rowcol;
+                            if (F32IO) *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(p.out) + oi) = OT[mt];
+                            else *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(p.out) + oi) = to_bf16(OT[mt]);
                         }
                     }
                 }
@@ -319,10 +507,11 @@ __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
                     Wh[mt] = sp.hi;
                     Wl[mt] = sp.lo;
                 }
-                const float bC = G[4 * CH];
+                const float bC = G[5 * CH];
 #pragma unroll
                 for (int nt = 0; nt < NTK; ++nt) S[nt] = bC * S[nt];
-                mgemm_tr<NTK, F32IO, true>(Kb, KPL, SK, Wh, Wl, NTC, g, c16, S);
+                mgemm_tr<DK, NTK, F32IO, true>(Kb, KPL, SK, Wh, Wl, NTC, g, c16, S);
+                split_state();  // for the next chunk, ahead of its barrier
             }
         }
         float* dst = mtile ? p.M_out : p.S_final;
@@ -335,7 +524,7 @@ __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
         }
     } else {
         // ---- A-waves: HBM -> register prefetch and register -> LDS commit of a chunk
-        TileRegs<CH, DK, F32IO, NTHA> pk, pq;
+        KQTile<CH, DK, F32IO, NTHA> pk, pq;
         TileRegs<CH, 16 * NB, F32IO, NTHA> pv;
         uint32_t pg = 0u, pb = 0u;  // gates stay raw bits until commit (no early wait on the loads)
         float lam_sum = 0.f;
@@ -379,17 +568,104 @@ __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
             }
         };
 
+        // Gated DeltaNet: (I + L_mm)^{-1} for every diagonal block mm, one wave.  The
+        // masked diagonal blocks go through LDS; then lane (g, c) solves column c of
+        // block g by right-looking forward substitution with the block in registers,
+        // so the 16 dependent steps wait on FMAs only.
+        auto diag_inverse = [&](int b, const float* gcw) {
+            if constexpr (FAM == FAM_GDN) {
+                const bf16* Kb = sK(b);
+                const float* G = sG(b);
+                float* INV = reinterpret_cast<float*>(smem + Ly::INV_OFF);
+                f32x4 acc[NTC];
+#pragma unroll
+                for (int mt = 0; mt < NTC; ++mt) acc[mt] = zero4();
+                if constexpr (NK == 1) {
+#pragma unroll
+                    for (int mt = 0; mt < NTC; ++mt) {
+                        const bf16* kr = Kb + (16 * mt + c16) * SK + 4 * g;
+                        acc[mt] = mma16(lds4(kr), lds4(kr), acc[mt]);
+                        if (F32IO) {
+                            acc[mt] = mma16(lds4(kr), lds4(kr + KPL), acc[mt]);
+                            acc[mt] = mma16(lds4(kr + KPL), lds4(kr), acc[mt]);
+                        }
+                    }
+                } else {
+                    constexpr int NKP = NK / 2;
+                    bf16x8 kv[NKP][NTC], lv[F32IO ? NKP : 1][NTC];
+#pragma unroll
+                    for (int kp = 0; kp < NKP; ++kp)
+#pragma unroll
+                        for (int mt = 0; mt < NTC; ++mt) {
+                            const bf16* kr = Kb + (16 * mt + c16) * SK + 32 * kp + 8 * g;
+                            kv[kp][mt] = lds8(kr);
+                            if constexpr (F32IO) lv[kp][mt] = lds8(kr + KPL);
+                        }
+                    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                    for (int kp = 0; kp < NKP; ++kp)
+#pragma unroll
+                        for (int mt = 0; mt < NTC; ++mt) {
+                            acc[mt] = mma32(kv[kp][mt], kv[kp][mt], acc[mt]);
+                            if constexpr (F32IO) {
+                                acc[mt] = mma32(kv[kp][mt], lv[kp][mt], acc[mt]);
+                                acc[mt] = mma32(lv[kp][mt], kv[kp][mt], acc[mt]);
+                            }
+                        }
+                }
+#pragma unroll
+                for (int mt = 0; mt < NTC; ++mt) {
+                    const float gci = gcw[16 * mt + c16];
+                    const f32x4 gt = lds4f(gcw + 16 * mt + 4 * g);
+                    const f32x4 bt = lds4f(G + CH + 16 * mt + 4 * g);
+                    f32x4 l;
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        l[r] = (c16 < 4 * g + r) ? bt[r] * __expf(gt[r] - gci) * acc[mt][r] : 0.f;
+                    // INV block mt: LTd[i][t] = L[t][i]
+                    *reinterpret_cast<f32x4*>(INV + mt * Ly::INV_BST + c16 * SLD + 4 * g) = l;
+                }
+                wave_lds_sync();
+                if (g < NTC) {
+                    const float* LTd = INV + g * Ly::INV_BST;
+                    f32x4 Lc[15][4];
+#pragma unroll
+                    for (int m = 0; m < 15; ++m)
+#pragma unroll
+                        for (int q4 = (m + 1) >> 2; q4 < 4; ++q4) Lc[m][q4] = lds4f(LTd + m * SLD + 4 * q4);
+                    float a[16], x[16];
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) a[i] = 0.f;
+#pragma unroll
+                    for (int m = 0; m < 16; ++m) {
+                        x[m] = (m == c16) ? 1.f : (m < c16 ? 0.f : -a[m]);
+                        if (m < 15) {
+#pragma unroll
+                            for (int i = m + 1; i < 16; ++i) a[i] += Lc[m][i >> 2][i & 3] * x[m];
+                        }
+                    }
+                    // NT[c][m] = N[m][c]: this lane's column is one contiguous NT row
+                    bf16* nt_hi = sNT(b) + g * BLK + c16 * SB;
+                    bf16* nt_lo = nt_hi + NTC * BLK;
+#pragma unroll
+                    for (int q4 = 0; q4 < 4; ++q4) {
+                        const Split4 sp = split4(f32x4{x[4 * q4], x[4 * q4 + 1], x[4 * q4 + 2], x[4 * q4 + 3]});
+                        *reinterpret_cast<bf16x4*>(nt_hi + 4 * q4) = sp.hi;
+                        *reinterpret_cast<bf16x4*>(nt_lo + 4 * q4) = sp.lo;
+                    }
+                }
+            }
+        };
+
         // A-waves: state-independent blocks of chunk ci into buffer ci & 1
         auto a_work = [&](int ci) {
             const int b = ci & 1;
             float* G = sG(b);
-            const bf16* Kb = sK(b);
-            const bf16* Qb = sQ(b);
             float* gcw = reinterpret_cast<float*>(smem + Ly::GC_OFF) + 64 * wa;
             // in-chunk cumulative log-gate, lane = token
             const float gate = lane < CH ? (FAM == FAM_GDN ? G[lane] : Ah * G[lane]) : 0.f;
-            const float gc = wave_incl_scan(gate, lane);
-            const float gtot = __shfl(gc, CH - 1, 64);
+            const float gc = wave_incl_scan(gate);
+            const float gtot = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, gc), CH - 1));
             gcw[lane] = gc;
             if (wa == 0) {
                 if (lane < CH) {
@@ -397,99 +673,29 @@ __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
                     const float wt = __expf(gtot - gc);
                     G[3 * CH + lane] = (FAM == FAM_GDN) ? wt : G[lane] * wt;
                 }
+                if (lane < CH) G[4 * CH + lane] = gc;
                 if (lane == 0) {
-                    G[4 * CH] = __expf(gtot);
-                    G[4 * CH + 1] = gtot;
+                    G[5 * CH] = __expf(gtot);
+                    G[5 * CH + 1] = gtot;
                 }
                 lam_sum += gtot;
             }
             wave_lds_sync();
-            // Gated DeltaNet: inverse of diagonal block wa of (I + L)
-            if (FAM == FAM_GDN && wa < NTC) {
-                const int mt = wa;
-                const bf16* kr = Kb + (16 * mt + c16) * SK;
-                const f32x4 acc = gemm_lds_lds<DK, F32IO>(kr, kr + KPL, kr, kr + KPL, g, zero4());
-                float* LTd = reinterpret_cast<float*>(smem + Ly::INV_OFF) + wa * 16 * SLD;
-                const float gci = gcw[16 * mt + c16];
-                f32x4 l;
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int t = 4 * g + r;  // local row; column c16
-                    l[r] = (c16 < t) ? G[CH + 16 * mt + t] * __expf(gcw[16 * mt + t] - gci) * acc[r] : 0.f;
-                }
-                *reinterpret_cast<f32x4*>(LTd + c16 * SLD + 4 * g) = l;  // LTd[i][t] = L[t][i]
-                wave_lds_sync();
-                // column c16 of (I + L_mm)^{-1}, right-looking forward substitution; each
-                // finished entry goes straight to NT[c16][m] = N[m][c16] (bf16 hi / lo)
-                bf16* nt_hi = sNT(b) + mt * BLK + c16 * SB;
-                bf16* nt_lo = nt_hi + NTC * BLK;
-                // the whole block in registers first (columns of L are rows of LTd), so the
-                // 16 dependent steps below wait on FMAs only, not on LDS
-                f32x4 Lc[15][4];
-#pragma unroll
-                for (int m = 0; m < 15; ++m)
-#pragma unroll
-                    for (int q4 = (m + 1) >> 2; q4 < 4; ++q4) Lc[m][q4] = lds4f(LTd + m * SLD + 4 * q4);
-                float a[16];
-#pragma unroll
-                for (int i = 0; i < 16; ++i) a[i] = 0.f;
-#pragma unroll
-                for (int m = 0; m < 16; ++m) {
-                    const float xm = (m == c16) ? 1.f : (m < c16 ? 0.f : -a[m]);
-                    if (g == 0) {
-                        const bf16 hi = (bf16)xm;
-                        nt_hi[m] = hi;
-                        nt_lo[m] = (bf16)(xm - (float)hi);
-                    }
-                    if (m < 15) {
-#pragma unroll
-                        for (int i = m + 1; i < 16; ++i) a[i] += Lc[m][i >> 2][i & 3] * xm;
-                    }
-                }
-            }
-            // token x token blocks: GDN strictly-lower K K^T blocks (negated L), then the
-            // output blocks Q K^T (GDN) / C B^T (SSD)
-            constexpr int N_OFFI = (FAM == FAM_GDN) ? NOFF : 0;
-            const int n_items = N_OFFI + (with_out ? NPB : 0);
-            for (int j = wa; j < n_items; j += NA) {
-                const bool is_l = j < N_OFFI;
-                int mt, nt;
-                if (is_l) {
-                    mt = 1;
-                    while (off_index(mt + 1, 0) <= j) ++mt;
-                    nt = j - off_index(mt, 0);
-                } else {
-                    const int jj = j - N_OFFI;
-                    mt = 0;
-                    while (low_index(mt + 1, 0) <= jj) ++mt;
-                    nt = jj - low_index(mt, 0);
-                }
-                const bf16* A = is_l ? Kb : Qb;
-                const bf16* ar = A + (16 * mt + c16) * SK;
-                const bf16* br = Kb + (16 * nt + c16) * SK;
-                const f32x4 acc = gemm_lds_lds<DK, F32IO>(ar, ar + KPL, br, br + KPL, g, zero4());
-                const int i = 16 * nt + c16;
-                const float gci = gcw[i];
-                f32x4 v;
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int t = 16 * mt + 4 * g + r;
-                    const float dec = __expf(gcw[t] - gci);
-                    if (is_l) v[r] = -G[CH + t] * dec * acc[r];  // nt < mt: every entry is below the diagonal
-                    else if (FAM == FAM_GDN) v[r] = (i <= t) ? p.scale * dec * acc[r] : 0.f;
-                    else v[r] = (i <= t) ? G[i] * dec * acc[r] : 0.f;
-                }
-                if (is_l) {
-                    store_tile_tr<SB, true>(sLT(b) + off_index(mt, nt) * BLK, NOFF * BLK, v, g, c16);
-                } else {
-                    store_tile_tr<SB, F32IO>(sPT(b) + low_index(mt, nt) * BLK, NPB * BLK, v, g, c16);
+            if constexpr (FAM == FAM_GDN) {
+                // A-wave 0 inverts the diagonal blocks; the others build the L blocks
+                using NS = integral_constant<int, NA - 1>;
+                switch (wa) {
+                    case 0: diag_inverse(b, gcw); break;
+                    case 1: items(integral_constant<int, 0>(), NS(), L_KIND(), b, gcw); break;
+                    case 2: items(integral_constant<int, 1>(), NS(), L_KIND(), b, gcw); break;
+                    default: items(integral_constant<int, 2>(), NS(), L_KIND(), b, gcw); break;
                 }
             }
         };
 
-        // prologue: chunk 0 staged and its blocks built; chunk 1 in flight.  Chunk
-        // c+1's loads are issued at the END of phase II and committed at the start
-        // of the next phase I, so they overlap the B-waves' remaining work.
+        // prologue: chunk 0 staged and its blocks built; chunk 1 in flight.  While
+        // the B-waves run chunk c, the A-waves commit chunk c+1 (loaded during
+        // chunk c-1), issue the loads of chunk c+2, and build chunk c+1's blocks.
         if (nch > 0) {
             prefetch(0);
             commit(0);
@@ -501,12 +707,12 @@ __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
         }
         for (int ci = 0; ci < nch; ++ci) {
             __syncthreads();
-            if (ci + 1 < nch) commit(ci + 1);
-            __syncthreads();
             if (ci + 1 < nch) {
-                a_work(ci + 1);
-                if (ci + 2 < nch) prefetch(ci + 2);
+                commit(ci + 1);
+                if (ci + 2 < nch) prefetch(ci + 2);  // a whole chunk of lead time
             }
+            __syncthreads();
+            if (ci + 1 < nch) a_work(ci + 1);
         }
         if (FAM == FAM_SSD && SUMMARY && p.M_out && tile == 0 && wa == 0 && lane == 0)
             p.M_out[int64_t(s) * p.h_v + h] = lam_sum;

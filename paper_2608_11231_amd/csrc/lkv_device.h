@@ -36,6 +36,19 @@ __device__ __forceinline__ f32x4 mma32(bf16x4 a0, bf16x4 a1, bf16x4 b0, bf16x4 b
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+// the same with one or both operands as a single 8-element fragment (see kq_pos)
+__device__ __forceinline__ f32x4 mma32(bf16x8 a, bf16x4 b0, bf16x4 b1, f32x4 c) {
+    bf16x8 b = __builtin_shufflevector(b0, b1, 0, 1, 2, 3, 4, 5, 6, 7);
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mma32(bf16x4 a0, bf16x4 a1, bf16x8 b, f32x4 c) {
+    bf16x8 a = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mma32(bf16x8 a, bf16x8 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
 // 16x16 output, contraction over one 16-slice
 __device__ __forceinline__ f32x4 mma16(bf16x4 a, bf16x4 b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(i16x4, a),
@@ -45,12 +58,21 @@ __device__ __forceinline__ f32x4 mma16(bf16x4 a, bf16x4 b, f32x4 c) {
 __device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
 __device__ __forceinline__ bf16x4 zero_bf16x4() { return bf16x4{(bf16)0.f, (bf16)0.f, (bf16)0.f, (bf16)0.f}; }
 
-// round-to-nearest-even fp32 -> bf16
-__device__ __forceinline__ bf16x4 to_bf16(f32x4 x) {
-    return bf16x4{(bf16)x[0], (bf16)x[1], (bf16)x[2], (bf16)x[3]};
+// round-to-nearest-even fp32 -> bf16, two values per conversion instruction
+// (packed through 32-bit words, so the pairs survive vector shuffles)
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{a, b}, bf16x2));
 }
+__device__ __forceinline__ bf16x4 to_bf16(f32x4 x) {
+    return __builtin_bit_cast(bf16x4, uint2{pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3])});
+}
+// exact bf16 -> fp32 from the packed bits (one shift or mask per value)
 __device__ __forceinline__ f32x4 to_f32(bf16x4 x) {
-    return f32x4{(float)x[0], (float)x[1], (float)x[2], (float)x[3]};
+    const uint2 b = __builtin_bit_cast(uint2, x);
+    return f32x4{__builtin_bit_cast(float, b.x << 16), __builtin_bit_cast(float, b.x & 0xffff0000u),
+                 __builtin_bit_cast(float, b.y << 16), __builtin_bit_cast(float, b.y & 0xffff0000u)};
 }
 
 // x = hi + lo with hi = bf16(x) and lo = bf16(x - hi); x - hi is exact in fp32,
@@ -65,8 +87,20 @@ __device__ __forceinline__ Split4 split4(f32x4 x) {
     return s;
 }
 
-// LDS loads of 4 consecutive elements (8 / 16 bytes)
+// LDS loads of 4 / 8 consecutive elements (8 / 16 / 16 bytes)
 __device__ __forceinline__ bf16x4 lds4(const bf16* p) { return *reinterpret_cast<const bf16x4*>(p); }
+__device__ __forceinline__ bf16x8 lds8(const bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
+
+// Column order of token-major K / Q tiles in LDS.  A 32-wide product needs, in
+// lane group g, the elements 4g..4g+3 and 16+4g..16+4g+3 of each 32-column slice
+// (the contraction bijection above).  Rows are stored with those two runs side
+// by side at 8g..8g+7, so one 16-byte read fetches a whole fragment; every
+// aligned run of 4 columns stays contiguous, so transposed reads still work.
+// Tiles only 16 columns wide keep the natural order.
+template <int DK>
+__device__ __forceinline__ constexpr int kq_pos(int d) {
+    return DK >= 32 ? ((d & ~31) | ((d & 12) << 1) | ((d & 16) >> 2) | (d & 3)) : d;
+}
 __device__ __forceinline__ f32x4 lds4f(const float* p) { return *reinterpret_cast<const f32x4*>(p); }
 
 // Transposed fragment read (gfx950 ds_read_b64_tr_b16).  Within each group of
@@ -84,13 +118,31 @@ __device__ __forceinline__ bf16x4 lds4_tr(const bf16* M, int stride, int r0, int
     return __builtin_bit_cast(bf16x4, v);
 }
 
-// Inclusive prefix sum across the 64 lanes of a wave.
-__device__ __forceinline__ float wave_incl_scan(float x, int lane) {
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        float y = __shfl_up(x, d, 64);
-        if (lane >= d) x += y;
-    }
+// lds4_tr for a K / Q tile stored in kq_pos order: column block c0 (a multiple of 16).
+template <int DK>
+__device__ __forceinline__ bf16x4 lds4_tr_kq(const bf16* M, int stride, int r0, int c0, int g, int c) {
+    const bf16* a = M + (r0 + 4 * g + (c >> 2)) * stride + kq_pos<DK>(c0 + 4 * (c & 3));
+    typedef __attribute__((address_space(3))) lds_i16x4 lds_ptr_t;
+    const lds_i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_ptr_t*)(a));
+    return __builtin_bit_cast(bf16x4, v);
+}
+
+// Inclusive prefix sum across the 64 lanes of a wave, in registers: shifts by
+// 1, 2, 4, 8 within each row of 16 lanes (DPP row_shr, zero-filled), then the
+// row totals are carried forward with DPP row_bcast:15 (into rows 1 and 3) and
+// row_bcast:31 (into rows 2 and 3).
+template <int CTRL, int ROW_MASK, bool BOUND_ZERO>
+__device__ __forceinline__ float dpp_mov(float x) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, ROW_MASK, 0xf,
+                                                                 BOUND_ZERO));
+}
+__device__ __forceinline__ float wave_incl_scan(float x) {
+    x += dpp_mov<0x111, 0xf, true>(x);  // row_shr:1
+    x += dpp_mov<0x112, 0xf, true>(x);  // row_shr:2
+    x += dpp_mov<0x114, 0xf, true>(x);  // row_shr:4
+    x += dpp_mov<0x118, 0xf, true>(x);  // row_shr:8
+    x += dpp_mov<0x142, 0xa, false>(x);  // row_bcast:15 -> rows 1, 3
+    x += dpp_mov<0x143, 0xc, false>(x);  // row_bcast:31 -> rows 2, 3
     return x;
 }
 
