@@ -93,60 +93,102 @@ hipError_t launch_compose_ssd(int32_t n_req, int32_t n_blk, int32_t H, int64_t p
 }
 
 // ---------------------------------------------------------------- Gated DeltaNet composition
-// Work unit = (request, head, tile of 16*nw state rows); wave w owns rows
+// Work unit = (request, head, tile of 16*NW state rows); wave w owns rows
 // row0 + 16w + (lane % 16).  The state stays in registers in acc-tile layout
 // (tile nt: S[row][16nt + 4g + r]), which is directly the B operand of
 //   S_new^T = M^T S^T    (contraction over the state's dk index),
 // so each step stages only M in LDS (row-major, split into bf16 hi/lo planes;
 // products Mh*Sh + Mh*Sl + Ml*Sh keep the fp32 chain at ~1e-5 relative) and
 // reads the M^T fragments with transposed LDS loads.
+//
+// The loop is software-pipelined: while block j is multiplied, the next
+// block's M (all of it, spread over the workgroup) and this lane's rows of its
+// B are already in flight from HBM into registers, so every step overlaps one
+// full block of loads with the products of the previous one.
 template <int DK>
 struct ComposeLds {
     static constexpr int SM = DK + 8;
     static __host__ __device__ constexpr size_t bytes() { return size_t(2) * DK * SM * 2; }
 };
 
-template <int DK>
-__global__ __launch_bounds__(256) void compose_gdn_kernel(ComposeArgs p) {
+template <int DK, int NW>
+__global__ __launch_bounds__(64 * NW) void compose_gdn_kernel(ComposeArgs p) {
     constexpr int NTK = DK / 16, SM = ComposeLds<DK>::SM;
+    constexpr int NTH = 64 * NW;
+    constexpr int NV = DK * DK / 4;              // float4 vectors of one M
+    constexpr int PER = (NV + NTH - 1) / NTH;    // of them per thread
     extern __shared__ __align__(16) char smem[];
     bf16* sMh = reinterpret_cast<bf16*>(smem);
     bf16* sMl = sMh + DK * SM;
-    const int nw = p.nw, nthreads = 64 * nw, tid = threadIdx.x;
+    const int tid = threadIdx.x;
     const int w = tid >> 6, lane = tid & 63, g = lane >> 4, c16 = lane & 15;
     const int u = xcd_unit(blockIdx.x, p.n_units);
     const int tile = u % p.tiles;
     const int h = (u / p.tiles) % p.h_v;
     const int r = u / (p.tiles * p.h_v);
-    const int my_row = tile * 16 * nw + 16 * w + c16;
+    const int my_row = tile * 16 * NW + 16 * w + c16;
 
     int32_t b0 = p.blk_cu[r], b1 = p.blk_cu[r + 1];
     b0 = b0 < 0 ? 0 : (b0 > p.n_ids ? p.n_ids : b0);
     b1 = b1 < b0 ? b0 : (b1 > p.n_ids ? p.n_ids : b1);
 
+    auto valid = [&](int32_t id) { return id >= 0 && id < p.n_blk; };
+    auto b_rows = [&](int32_t id) {
+        return p.B_pool + (((int64_t)id * p.h_v + h) * p.dv + my_row) * DK + 4 * g;
+    };
+    f32x4 mreg[PER], breg[NTK];
+    auto prefetch = [&](int32_t id) {
+        const f32x4* Mj = reinterpret_cast<const f32x4*>(p.M_pool + ((int64_t)id * p.h_v + h) * DK * DK);
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int idx = tid + i * NTH;
+            if (NV % NTH == 0 || idx < NV) mreg[i] = Mj[idx];  // shared by the head's row tiles (L2)
+        }
+        const float* Bj = b_rows(id);
+#pragma unroll
+        for (int nt = 0; nt < NTK; ++nt)
+            breg[nt] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(Bj + 16 * nt));
+    };
+
     f32x4 S[NTK];
 #pragma unroll
     for (int nt = 0; nt < NTK; ++nt) S[nt] = zero4();
     bool bad = false;
-    for (int32_t j = b0; j < b1; ++j) {
-        const int32_t id = p.blk_ids[j];
-        if (id < 0 || id >= p.n_blk) { bad = true; break; }
-        const float* Bj = p.B_pool + (((int64_t)id * p.h_v + h) * p.dv + my_row) * DK + 4 * g;
-        if (j == b0) {
+    if (b0 < b1) {
+        const int32_t id0 = p.blk_ids[b0];
+        if (!valid(id0)) {
+            bad = true;
+        } else {
+            const float* B0 = b_rows(id0);
 #pragma unroll
-            for (int nt = 0; nt < NTK; ++nt) S[nt] = *reinterpret_cast<const f32x4*>(Bj + 16 * nt);
-            continue;
+            for (int nt = 0; nt < NTK; ++nt) S[nt] = *reinterpret_cast<const f32x4*>(B0 + 16 * nt);
         }
-        // stage M row-major, split into bf16 hi / lo planes (16-byte reads, 8-byte writes)
-        const float* Mj = p.M_pool + ((int64_t)id * p.h_v + h) * DK * DK;
+    }
+    int32_t id_next = (!bad && b0 + 1 < b1) ? p.blk_ids[b0 + 1] : 0;
+    if (!bad && b0 + 1 < b1 && valid(id_next)) prefetch(id_next);
+    for (int32_t j = b0 + 1; j < b1 && !bad; ++j) {
+        if (!valid(id_next)) {  // uniform over the workgroup: every wave leaves together
+            bad = true;
+            break;
+        }
+        // stage M_j (prefetched) row-major, split into bf16 hi / lo planes
         __syncthreads();
-        for (int idx = tid; idx < DK * DK / 4; idx += nthreads) {
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int idx = tid + i * NTH;
+            if (NV % NTH != 0 && idx >= NV) continue;
             const int ii = idx / (DK / 4), jj = (idx % (DK / 4)) * 4;
-            const Split4 sp = split4(*reinterpret_cast<const f32x4*>(Mj + ii * DK + jj));
+            const Split4 sp = split4(mreg[i]);
             *reinterpret_cast<bf16x4*>(sMh + ii * SM + jj) = sp.hi;
             *reinterpret_cast<bf16x4*>(sMl + ii * SM + jj) = sp.lo;
         }
+        f32x4 acc[NTK];
+#pragma unroll
+        for (int nt = 0; nt < NTK; ++nt) acc[nt] = breg[nt];
         __syncthreads();
+        // the next block's loads go out before this block's products
+        id_next = j + 1 < b1 ? p.blk_ids[j + 1] : 0;
+        if (j + 1 < b1 && valid(id_next)) prefetch(id_next);
         bf16x4 Sh[NTK], Sl[NTK];
 #pragma unroll
         for (int nt = 0; nt < NTK; ++nt) {
@@ -154,31 +196,36 @@ __global__ __launch_bounds__(256) void compose_gdn_kernel(ComposeArgs p) {
             Sh[nt] = sp.hi;
             Sl[nt] = sp.lo;
         }
-        // S_new^T tile nt (rows j = 16nt..16nt+15) = M^T S^T: A fragments of M^T come
-        // straight from the row-major planes through transposed LDS reads
+        // S_new^T tile nt (rows 16nt..16nt+15) = M^T S^T + B^T: A fragments of M^T
+        // come straight from the row-major planes through transposed LDS reads;
+        // the dk tiles are interleaved so NTK accumulation chains are in flight
+        if constexpr (NTK == 1) {
+            const bf16x4 a0 = lds4_tr(sMh, SM, 0, 0, g, c16);
+            const bf16x4 c0 = lds4_tr(sMl, SM, 0, 0, g, c16);
+            acc[0] = mma16(a0, Sh[0], acc[0]);
+            acc[0] = mma16(a0, Sl[0], acc[0]);
+            acc[0] = mma16(c0, Sh[0], acc[0]);
+        } else {
 #pragma unroll
-        for (int nt = 0; nt < NTK; ++nt) {
-            f32x4 acc = *reinterpret_cast<const f32x4*>(Bj + 16 * nt);
-            int kg = 0;
+            for (int kg = 0; kg < NTK; kg += 2) {
+                bf16x4 a0[NTK], a1[NTK], c0[NTK], c1[NTK];
 #pragma unroll
-            for (; kg + 1 < NTK; kg += 2) {
-                const bf16x4 a0 = lds4_tr(sMh, SM, 16 * kg, 16 * nt, g, c16);
-                const bf16x4 a1 = lds4_tr(sMh, SM, 16 * kg + 16, 16 * nt, g, c16);
-                const bf16x4 c0 = lds4_tr(sMl, SM, 16 * kg, 16 * nt, g, c16);
-                const bf16x4 c1 = lds4_tr(sMl, SM, 16 * kg + 16, 16 * nt, g, c16);
-                acc = mma32(a0, a1, Sh[kg], Sh[kg + 1], acc);
-                acc = mma32(a0, a1, Sl[kg], Sl[kg + 1], acc);
-                acc = mma32(c0, c1, Sh[kg], Sh[kg + 1], acc);
+                for (int nt = 0; nt < NTK; ++nt) {
+                    a0[nt] = lds4_tr(sMh, SM, 16 * kg, 16 * nt, g, c16);
+                    a1[nt] = lds4_tr(sMh, SM, 16 * kg + 16, 16 * nt, g, c16);
+                    c0[nt] = lds4_tr(sMl, SM, 16 * kg, 16 * nt, g, c16);
+                    c1[nt] = lds4_tr(sMl, SM, 16 * kg + 16, 16 * nt, g, c16);
+                }
+#pragma unroll
+                for (int nt = 0; nt < NTK; ++nt) {
+                    acc[nt] = mma32(a0[nt], a1[nt], Sh[kg], Sh[kg + 1], acc[nt]);
+                    acc[nt] = mma32(a0[nt], a1[nt], Sl[kg], Sl[kg + 1], acc[nt]);
+                    acc[nt] = mma32(c0[nt], c1[nt], Sh[kg], Sh[kg + 1], acc[nt]);
+                }
             }
-            if (NTK & 1) {
-                const bf16x4 a0 = lds4_tr(sMh, SM, 16 * kg, 16 * nt, g, c16);
-                const bf16x4 c0 = lds4_tr(sMl, SM, 16 * kg, 16 * nt, g, c16);
-                acc = mma16(a0, Sh[kg], acc);
-                acc = mma16(a0, Sl[kg], acc);
-                acc = mma16(c0, Sh[kg], acc);
-            }
-            S[nt] = acc;
         }
+#pragma unroll
+        for (int nt = 0; nt < NTK; ++nt) S[nt] = acc[nt];
     }
     if (bad) {
         const float f = __builtin_nanf("");
@@ -200,15 +247,25 @@ size_t compose_gdn_lds_bytes(int dk) {
     return 0;
 }
 
-template <int DK>
-static hipError_t launch_compose_gdn_t(const ComposeArgs& a, hipStream_t st) {
+template <int DK, int NW>
+static hipError_t launch_compose_gdn_nw(const ComposeArgs& a, hipStream_t st) {
     const size_t lds = ComposeLds<DK>::bytes();
-    auto kern = compose_gdn_kernel<DK>;
+    auto kern = compose_gdn_kernel<DK, NW>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kern, dim3(a.n_units), dim3(64 * a.nw), lds, st, a);
+    hipLaunchKernelGGL(kern, dim3(a.n_units), dim3(64 * NW), lds, st, a);
     return hipGetLastError();
+}
+
+template <int DK>
+static hipError_t launch_compose_gdn_t(const ComposeArgs& a, hipStream_t st) {
+    switch (a.nw) {
+        case 1: return launch_compose_gdn_nw<DK, 1>(a, st);
+        case 2: return launch_compose_gdn_nw<DK, 2>(a, st);
+        case 4: return launch_compose_gdn_nw<DK, 4>(a, st);
+    }
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_compose_gdn(int dk, const ComposeArgs& a, hipStream_t st) {
