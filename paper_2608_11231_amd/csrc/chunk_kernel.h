@@ -24,10 +24,14 @@
 // software pipeline over chunks:
 //   * A-waves (NA = 4): stage chunk c+1 from registers into LDS and prefetch
 //     chunk c+2 from HBM; then compute chunk c+1's state-independent blocks,
-//     stored pre-split (bf16 hi/lo) and transposed for direct fragment reads;
+//     stored pre-split (bf16 hi/lo) and transposed for direct fragment reads:
+//     the masked 16x16 diagonal blocks of I + L and the strictly-lower L blocks.
+//     For Gated DeltaNet one A-wave does not stage: while the B-waves start
+//     chunk c it inverts chunk c's diagonal blocks and combines them into the
+//     off-diagonal blocks of the two 32x32 diagonal blocks of (I + L)^{-1};
 //   * B-waves (NB, 16 state rows each): chunk c's state chain -- K S^T, the
-//     block forward substitution for U, the outputs, the state update -- with
-//     the fp32 state held in MFMA accumulator registers throughout.
+//     two-level block substitution for U (32-token halves), the outputs, the
+//     state update -- with the fp32 state held in MFMA accumulator registers.
 // LDS holds two pipeline buffers; two workgroup barriers per chunk.
 //
 // Precision: bf16 inputs enter the matrix cores exactly.  fp32 operands of the
@@ -94,6 +98,8 @@ struct ChunkLds {
     static constexpr size_t LT_SZ = HAS_L ? al(size_t(NOFF) * BLK * 2 * 2) : 0;
     static constexpr size_t NT_SZ = HAS_L ? al(size_t(NTC) * BLK * 2 * 2) : 0;
     static constexpr size_t PT_SZ = HAS_Q ? al(size_t(NPB) * BLK * PL * 2) : 0;
+    // off-diagonal blocks T_10, T_32 of the two 32x32 diagonal blocks of (I + L)^{-1}, hi / lo
+    static constexpr size_t TT_SZ = (HAS_L && NTC == 4) ? al(size_t(2) * BLK * 2 * 2) : 0;
     static constexpr size_t K_OFF = 0;
     static constexpr size_t Q_OFF = K_OFF + K_SZ;
     static constexpr size_t V_OFF = Q_OFF + Q_SZ;
@@ -101,7 +107,8 @@ struct ChunkLds {
     static constexpr size_t LT_OFF = G_OFF + G_SZ;
     static constexpr size_t NT_OFF = LT_OFF + LT_SZ;
     static constexpr size_t PT_OFF = NT_OFF + NT_SZ;
-    static constexpr size_t BUF = PT_OFF + PT_SZ;  // one pipeline buffer
+    static constexpr size_t TT_OFF = PT_OFF + PT_SZ;
+    static constexpr size_t BUF = TT_OFF + TT_SZ;  // one pipeline buffer
     static constexpr size_t GC_OFF = 2 * BUF;      // per A-wave gate prefix
     static constexpr size_t INV_OFF = GC_OFF + al(NA * 64 * 4);
     static constexpr int INV_BST = 16 * SLD + 4;      // f32 stride of inverse scratch blocks (bank shift)
@@ -126,14 +133,17 @@ __device__ __forceinline__ constexpr int low_mt(int j) {
 template <int FAM, int DK, int CH, bool F32IO, int NB, bool SUMMARY>
 __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
     using Ly = ChunkLds<FAM, DK, CH, F32IO, NB, SUMMARY>;
-    constexpr int NTC = CH / 16, NTK = DK / 16, NTHA = 64 * NA;
+    constexpr int NTC = CH / 16, NTK = DK / 16;
     constexpr int SK = Ly::SK, SV = Ly::SV, SB = Ly::SB, BLK = Ly::BLK, SLD = Ly::SLD;
     constexpr int NOFF = Ly::NOFF, NPB = Ly::NPB;
     constexpr int KPL = CH * SK, VPL = CH * SV;  // lo-plane offsets (fp32 io)
     extern __shared__ __align__(16) char smem[];
 
     const int tid = threadIdx.x;
-    const int w = tid >> 6, lane = tid & 63, g = lane >> 4, c16 = lane & 15;
+    // wave index as a scalar: role and slot branches below are then uniform
+    // scalar branches instead of exec-masked divergent regions
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int lane = tid & 63, g = lane >> 4, c16 = lane & 15;
     const bool is_b = w < NB;
     const int wa = w - NB;            // A-wave index
     const int tid_a = tid - 64 * NB;  // thread index among the A-waves
@@ -163,6 +173,7 @@ __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
     auto sLT = [&](int b) { return reinterpret_cast<bf16*>(smem + b * Ly::BUF + Ly::LT_OFF); };
     auto sNT = [&](int b) { return reinterpret_cast<bf16*>(smem + b * Ly::BUF + Ly::NT_OFF); };
     auto sPT = [&](int b) { return reinterpret_cast<bf16*>(smem + b * Ly::BUF + Ly::PT_OFF); };
+    auto sTT = [&](int b) { return reinterpret_cast<bf16*>(smem + b * Ly::BUF + Ly::TT_OFF); };
 
     // ---- state-independent token blocks of one chunk (buffer b).  Items are the
     // 16x16 blocks: the strictly-lower K K^T blocks of Gated DeltaNet (kind L,
@@ -395,54 +406,74 @@ __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
                             Pf[pl][j] = lds4_tr(sPT(b) + pl * NPB * BLK + j * BLK, SB, 0, 0, g, c16);
                 }
                 if (FAM == FAM_GDN) {
-                    // U_mt = N_mt (beta X_mt - sum_{m<mt} L_{mt,m} U_m)   (blocks of 16 tokens);
-                    // the hi*hi and the correction passes accumulate apart.  All L and N
-                    // fragments are in registers before the dependent chain starts.
+                    // U = (I + L)^{-1} X over 32-token halves A = blocks {0, 1}, B = {2, 3}:
+                    //   U_A = T_A X_A,  U_B = T_B (X_B - L_BA U_A),
+                    // with T_A = [[N_0, 0], [T_10, N_1]], T_B = [[N_2, 0], [T_32, N_3]] (the
+                    // 16x16 diagonal inverses N and T_10 = -N_1 L_10 N_0, T_32 = -N_3 L_32 N_2
+                    // come from the A-waves).  Three dependent stages; the hi*hi and the
+                    // correction passes accumulate apart.  All fragments are requested
+                    // before the first product.
                     const bf16* LT = sLT(b);
                     const bf16* NT = sNT(b);
-                    bf16x4 Lh[NOFF > 0 ? NOFF : 1], Ll[NOFF > 0 ? NOFF : 1], Nh[NTC], Nl[NTC];
-#pragma unroll
-                    for (int j = 0; j < NOFF; ++j) {
-                        Lh[j] = lds4_tr(LT + j * BLK, SB, 0, 0, g, c16);
-                        Ll[j] = lds4_tr(LT + (NOFF + j) * BLK, SB, 0, 0, g, c16);
-                    }
+                    bf16x4 Nh[NTC], Nl[NTC];
 #pragma unroll
                     for (int mt = 0; mt < NTC; ++mt) {
                         Nh[mt] = lds4_tr(NT + mt * BLK, SB, 0, 0, g, c16);
                         Nl[mt] = lds4_tr(NT + (NTC + mt) * BLK, SB, 0, 0, g, c16);
                     }
-                    // sum over token blocks kg < mt of A_{mt,kg} B_kg: pairs through the
-                    // 32-wide MFMA, a lone block through the 16-wide one, an odd tail after
-                    // pairs zero-padded (one shape per chain)
-                    auto blk_sum = [&](const bf16x4* A, const bf16x4* B, int mt, f32x4 acc) {
-                        int kg = 0;
-#pragma unroll
-                        for (; kg + 1 < mt; kg += 2)
-                            acc = mma32(A[off_index(mt, kg)], A[off_index(mt, kg + 1)], B[kg], B[kg + 1], acc);
-                        if (kg < mt) {
-                            if (kg == 0) {
-                                acc = mma16(A[off_index(mt, kg)], B[kg], acc);
-                            } else {
-                                const bf16x4 z = zero_bf16x4();
-                                acc = mma32(A[off_index(mt, kg)], z, B[kg], z, acc);
-                            }
-                        }
-                        return acc;
-                    };
-#pragma unroll
-                    for (int mt = 0; mt < NTC; ++mt) {
-                        const f32x4 a0 = blk_sum(Lh, Uh, mt, X[mt]);
-                        f32x4 a1 = blk_sum(Lh, Ul, mt, zero4());
-                        a1 = blk_sum(Ll, Uh, mt, a1);
-                        const Split4 rs = split4(a0 + a1);
-                        const bf16x4 nh = Nh[mt], nl = Nl[mt];
-                        f32x4 u0 = mma16(nh, rs.hi, zero4());
-                        f32x4 u1 = mma16(nh, rs.lo, zero4());
-                        u1 = mma16(nl, rs.hi, u1);
-                        U[mt] = u0 + u1;
-                        const Split4 us = split4(U[mt]);
+                    auto split_u = [&](int mt, f32x4 v) {
+                        U[mt] = v;
+                        const Split4 us = split4(v);
                         Uh[mt] = us.hi;
                         Ul[mt] = us.lo;
+                    };
+                    if constexpr (NTC == 1) {
+                        const Split4 xs = split4(X[0]);
+                        const f32x4 u0 = mma16(Nh[0], xs.hi, zero4());
+                        f32x4 u1 = mma16(Nh[0], xs.lo, zero4());
+                        u1 = mma16(Nl[0], xs.hi, u1);
+                        split_u(0, u0 + u1);
+                    } else {
+                        static_assert(NTC == 4, "chunk of 16 or 64 tokens");
+                        const bf16* TT = sTT(b);
+                        const bf16x4 t10h = lds4_tr(TT, SB, 0, 0, g, c16);
+                        const bf16x4 t32h = lds4_tr(TT + BLK, SB, 0, 0, g, c16);
+                        const bf16x4 t10l = lds4_tr(TT + 2 * BLK, SB, 0, 0, g, c16);
+                        const bf16x4 t32l = lds4_tr(TT + 3 * BLK, SB, 0, 0, g, c16);
+                        // -L_20, -L_21, -L_30, -L_31 (strictly-lower blocks 1..4), hi / lo
+                        bf16x4 Lh[4], Ll[4];
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) {
+                            Lh[j] = lds4_tr(LT + (1 + j) * BLK, SB, 0, 0, g, c16);
+                            Ll[j] = lds4_tr(LT + (NOFF + 1 + j) * BLK, SB, 0, 0, g, c16);
+                        }
+                        // stage 1: U_0 = N_0 X_0, U_1 = T_10 X_0 + N_1 X_1
+                        const Split4 x0 = split4(X[0]), x1 = split4(X[1]);
+                        const f32x4 u0h = mma16(Nh[0], x0.hi, zero4());
+                        const f32x4 u1h = mma32(t10h, Nh[1], x0.hi, x1.hi, zero4());
+                        f32x4 u0l = mma16(Nh[0], x0.lo, zero4());
+                        f32x4 u1l = mma32(t10h, Nh[1], x0.lo, x1.lo, zero4());
+                        u0l = mma16(Nl[0], x0.hi, u0l);
+                        u1l = mma32(t10l, Nl[1], x0.hi, x1.hi, u1l);
+                        split_u(0, u0h + u0l);
+                        split_u(1, u1h + u1l);
+                        // stage 2: R_2 = X_2 - L_20 U_0 - L_21 U_1, R_3 = X_3 - L_30 U_0 - L_31 U_1
+                        const f32x4 r2h = mma32(Lh[0], Lh[1], Uh[0], Uh[1], X[2]);
+                        const f32x4 r3h = mma32(Lh[2], Lh[3], Uh[0], Uh[1], X[3]);
+                        f32x4 r2l = mma32(Lh[0], Lh[1], Ul[0], Ul[1], zero4());
+                        f32x4 r3l = mma32(Lh[2], Lh[3], Ul[0], Ul[1], zero4());
+                        r2l = mma32(Ll[0], Ll[1], Uh[0], Uh[1], r2l);
+                        r3l = mma32(Ll[2], Ll[3], Uh[0], Uh[1], r3l);
+                        const Split4 x2 = split4(r2h + r2l), x3 = split4(r3h + r3l);
+                        // stage 3: U_2 = N_2 R_2, U_3 = T_32 R_2 + N_3 R_3
+                        const f32x4 u2h = mma16(Nh[2], x2.hi, zero4());
+                        const f32x4 u3h = mma32(t32h, Nh[3], x2.hi, x3.hi, zero4());
+                        f32x4 u2l = mma16(Nh[2], x2.lo, zero4());
+                        f32x4 u3l = mma32(t32h, Nh[3], x2.lo, x3.lo, zero4());
+                        u2l = mma16(Nl[2], x2.hi, u2l);
+                        u3l = mma32(t32l, Nl[3], x2.hi, x3.hi, u3l);
+                        split_u(2, u2h + u2l);
+                        split_u(3, u3h + u3l);
                     }
                 } else {
 #pragma unroll
@@ -524,8 +555,12 @@ __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
         }
     } else {
         // ---- A-waves: HBM -> register prefetch and register -> LDS commit of a chunk
-        KQTile<CH, DK, F32IO, NTHA> pk, pq;
-        TileRegs<CH, 16 * NB, F32IO, NTHA> pv;
+        // Gated DeltaNet: A-waves 0..NA-2 stage tiles; A-wave NA-1 (the solver)
+        // finishes the triangular blocks of the chunk the B-waves are working on.
+        constexpr int NSTG = (FAM == FAM_GDN) ? NA - 1 : NA;
+        const bool stager = wa < NSTG;
+        KQTile<CH, DK, F32IO, 64 * NSTG> pk, pq;
+        TileRegs<CH, 16 * NB, F32IO, 64 * NSTG> pv;
         uint32_t pg = 0u, pb = 0u;  // gates stay raw bits until commit (no early wait on the loads)
         float lam_sum = 0.f;
         constexpr int ES = F32IO ? 4 : 2;
@@ -568,66 +603,57 @@ __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
             }
         };
 
-        // Gated DeltaNet: (I + L_mm)^{-1} for every diagonal block mm, one wave.  The
-        // masked diagonal blocks go through LDS; then lane (g, c) solves column c of
-        // block g by right-looking forward substitution with the block in registers,
-        // so the 16 dependent steps wait on FMAs only.
-        auto diag_inverse = [&](int b, const float* gcw) {
+        // Gated DeltaNet: (I + L_mm)^{-1} of the diagonal blocks.  diag_prep (A-wave
+        // mm, while the chunk's other blocks are built) puts the masked diagonal
+        // block mm in LDS; in the next phase the solver wave inverts all of them
+        // by right-looking forward substitution with each block in registers, so
+        // the 16 dependent steps wait on FMAs only.
+        auto diag_prep = [&](int b, const float* gcw, int mt) {
             if constexpr (FAM == FAM_GDN) {
-                const bf16* Kb = sK(b);
+                const bf16* kr = sK(b) + (16 * mt + c16) * SK;
                 const float* G = sG(b);
-                float* INV = reinterpret_cast<float*>(smem + Ly::INV_OFF);
-                f32x4 acc[NTC];
-#pragma unroll
-                for (int mt = 0; mt < NTC; ++mt) acc[mt] = zero4();
+                float* INV = reinterpret_cast<float*>(smem + Ly::INV_OFF) + mt * Ly::INV_BST;
+                f32x4 acc = zero4();
                 if constexpr (NK == 1) {
-#pragma unroll
-                    for (int mt = 0; mt < NTC; ++mt) {
-                        const bf16* kr = Kb + (16 * mt + c16) * SK + 4 * g;
-                        acc[mt] = mma16(lds4(kr), lds4(kr), acc[mt]);
-                        if (F32IO) {
-                            acc[mt] = mma16(lds4(kr), lds4(kr + KPL), acc[mt]);
-                            acc[mt] = mma16(lds4(kr + KPL), lds4(kr), acc[mt]);
-                        }
+                    acc = mma16(lds4(kr + 4 * g), lds4(kr + 4 * g), acc);
+                    if (F32IO) {
+                        acc = mma16(lds4(kr + 4 * g), lds4(kr + KPL + 4 * g), acc);
+                        acc = mma16(lds4(kr + KPL + 4 * g), lds4(kr + 4 * g), acc);
                     }
                 } else {
                     constexpr int NKP = NK / 2;
-                    bf16x8 kv[NKP][NTC], lv[F32IO ? NKP : 1][NTC];
+                    bf16x8 kv[NKP], lv[F32IO ? NKP : 1];
 #pragma unroll
-                    for (int kp = 0; kp < NKP; ++kp)
-#pragma unroll
-                        for (int mt = 0; mt < NTC; ++mt) {
-                            const bf16* kr = Kb + (16 * mt + c16) * SK + 32 * kp + 8 * g;
-                            kv[kp][mt] = lds8(kr);
-                            if constexpr (F32IO) lv[kp][mt] = lds8(kr + KPL);
-                        }
+                    for (int kp = 0; kp < NKP; ++kp) {
+                        kv[kp] = lds8(kr + 32 * kp + 8 * g);
+                        if constexpr (F32IO) lv[kp] = lds8(kr + KPL + 32 * kp + 8 * g);
+                    }
                     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                    for (int kp = 0; kp < NKP; ++kp)
-#pragma unroll
-                        for (int mt = 0; mt < NTC; ++mt) {
-                            acc[mt] = mma32(kv[kp][mt], kv[kp][mt], acc[mt]);
-                            if constexpr (F32IO) {
-                                acc[mt] = mma32(kv[kp][mt], lv[kp][mt], acc[mt]);
-                                acc[mt] = mma32(lv[kp][mt], kv[kp][mt], acc[mt]);
-                            }
+                    for (int kp = 0; kp < NKP; ++kp) {
+                        acc = mma32(kv[kp], kv[kp], acc);
+                        if constexpr (F32IO) {
+                            acc = mma32(kv[kp], lv[kp], acc);
+                            acc = mma32(lv[kp], kv[kp], acc);
                         }
+                    }
                 }
+                const float gci = gcw[16 * mt + c16];
+                const f32x4 gt = lds4f(gcw + 16 * mt + 4 * g);
+                const f32x4 bt = lds4f(G + CH + 16 * mt + 4 * g);
+                f32x4 l;
 #pragma unroll
-                for (int mt = 0; mt < NTC; ++mt) {
-                    const float gci = gcw[16 * mt + c16];
-                    const f32x4 gt = lds4f(gcw + 16 * mt + 4 * g);
-                    const f32x4 bt = lds4f(G + CH + 16 * mt + 4 * g);
-                    f32x4 l;
-#pragma unroll
-                    for (int r = 0; r < 4; ++r)
-                        l[r] = (c16 < 4 * g + r) ? bt[r] * __expf(gt[r] - gci) * acc[mt][r] : 0.f;
-                    // INV block mt: LTd[i][t] = L[t][i]
-                    *reinterpret_cast<f32x4*>(INV + mt * Ly::INV_BST + c16 * SLD + 4 * g) = l;
-                }
-                wave_lds_sync();
+                for (int r = 0; r < 4; ++r) l[r] = (c16 < 4 * g + r) ? bt[r] * __expf(gt[r] - gci) * acc[r] : 0.f;
+                // LTd[i][t] = L[t][i]
+                *reinterpret_cast<f32x4*>(INV + c16 * SLD + 4 * g) = l;
+            }
+        };
+        // One wave inverts every diagonal block: lane c of lane group g solves
+        // column c of block g (the masked blocks were left in LDS by diag_prep).
+        auto diag_solve_all = [&](int b) {
+            if constexpr (FAM == FAM_GDN) {
                 if (g < NTC) {
-                    const float* LTd = INV + g * Ly::INV_BST;
+                    const float* LTd = reinterpret_cast<const float*>(smem + Ly::INV_OFF) + g * Ly::INV_BST;
                     f32x4 Lc[15][4];
 #pragma unroll
                     for (int m = 0; m < 15; ++m)
@@ -653,6 +679,48 @@ __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
                         *reinterpret_cast<bf16x4*>(nt_hi + 4 * q4) = sp.hi;
                         *reinterpret_cast<bf16x4*>(nt_lo + 4 * q4) = sp.lo;
                     }
+                    asm volatile("" ::: "memory");  // keep the stores in this branch
+                }
+                wave_lds_sync();  // N is read back by t_blocks
+            }
+        };
+
+        // Gated DeltaNet, 64-token chunks: T_10 = -N_1 L_10 N_0 and T_32 = -N_3 L_32 N_2,
+        // the off-diagonal blocks of the 32x32 diagonal blocks of (I + L)^{-1}, from the
+        // stored -L and N blocks of buffer b.  Y = (-L)^T N_i^T = -(N_i L)^T, whose acc
+        // layout is the A operand of -N_i L; then T = (-N_i L) N_{i-1}.  fp32 products as
+        // hi / lo passes; T goes to LDS transposed, like N.
+        auto t_blocks = [&](int b) {
+            if constexpr (FAM == FAM_GDN && NTC == 4) {
+                const bf16* LT = sLT(b);
+                const bf16* NT = sNT(b);
+                bf16* TT = sTT(b);
+                constexpr int JL[2] = {off_index(1, 0), off_index(3, 2)};
+                f32x4 y[2];
+#pragma unroll
+                for (int q = 0; q < 2; ++q) {
+                    const int i = 2 * q + 1, j = JL[q];
+                    // (-L)^T as A: (-L)[4g+r][c] = XT[c][4g+r], a plain read of XT row c
+                    const bf16x4 lh = lds4(LT + j * BLK + c16 * SB + 4 * g);
+                    const bf16x4 ll = lds4(LT + (NOFF + j) * BLK + c16 * SB + 4 * g);
+                    // N_i^T as B: N_i[c][4g+r] = NT[4g+r][c], a transposed read
+                    const bf16x4 nh = lds4_tr(NT + i * BLK, SB, 0, 0, g, c16);
+                    const bf16x4 nl = lds4_tr(NT + (NTC + i) * BLK, SB, 0, 0, g, c16);
+                    f32x4 acc = mma16(lh, nh, zero4());
+                    acc = mma16(lh, nl, acc);
+                    y[q] = mma16(ll, nh, acc);
+                }
+#pragma unroll
+                for (int q = 0; q < 2; ++q) {
+                    const int i = 2 * q + 1;
+                    // N_{i-1} as B: N[4g+r][c] = NT[c][4g+r], a plain read
+                    const bf16x4 nh = lds4(NT + (i - 1) * BLK + c16 * SB + 4 * g);
+                    const bf16x4 nl = lds4(NT + (NTC + i - 1) * BLK + c16 * SB + 4 * g);
+                    const Split4 ys = split4(y[q]);
+                    f32x4 t = mma16(ys.hi, nh, zero4());
+                    t = mma16(ys.hi, nl, t);
+                    t = mma16(ys.lo, nh, t);
+                    store_tile_tr<SB, true>(TT + q * BLK, 2 * BLK, t, g, c16);
                 }
             }
         };
@@ -682,13 +750,14 @@ __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
             }
             wave_lds_sync();
             if constexpr (FAM == FAM_GDN) {
-                // A-wave 0 inverts the diagonal blocks; the others build the L blocks
-                using NS = integral_constant<int, NA - 1>;
+                // A-wave a masks diagonal block a and builds L blocks a, a + 4, ...
+                if (wa < NTC) diag_prep(b, gcw, wa);
+                using NS = integral_constant<int, NA>;
                 switch (wa) {
-                    case 0: diag_inverse(b, gcw); break;
-                    case 1: items(integral_constant<int, 0>(), NS(), L_KIND(), b, gcw); break;
-                    case 2: items(integral_constant<int, 1>(), NS(), L_KIND(), b, gcw); break;
-                    default: items(integral_constant<int, 2>(), NS(), L_KIND(), b, gcw); break;
+                    case 0: items(integral_constant<int, 0>(), NS(), L_KIND(), b, gcw); break;
+                    case 1: items(integral_constant<int, 1>(), NS(), L_KIND(), b, gcw); break;
+                    case 2: items(integral_constant<int, 2>(), NS(), L_KIND(), b, gcw); break;
+                    default: items(integral_constant<int, 3>(), NS(), L_KIND(), b, gcw); break;
                 }
             }
         };
@@ -696,23 +765,36 @@ __global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
         // prologue: chunk 0 staged and its blocks built; chunk 1 in flight.  While
         // the B-waves run chunk c, the A-waves commit chunk c+1 (loaded during
         // chunk c-1), issue the loads of chunk c+2, and build chunk c+1's blocks.
-        if (nch > 0) {
-            prefetch(0);
-            commit(0);
-        }
-        __syncthreads();
-        if (nch > 0) {
-            a_work(0);
-            if (nch > 1) prefetch(1);
-        }
-        for (int ci = 0; ci < nch; ++ci) {
-            __syncthreads();
-            if (ci + 1 < nch) {
-                commit(ci + 1);
-                if (ci + 2 < nch) prefetch(ci + 2);  // a whole chunk of lead time
+        // The stagers and the solver also run separate loops (same barrier
+        // sequence), so the solver's registers do not overlap the prefetch ones.
+        if (stager) {
+            if (nch > 0) {
+                prefetch(0);
+                commit(0);
             }
             __syncthreads();
-            if (ci + 1 < nch) a_work(ci + 1);
+            if (nch > 0) {
+                a_work(0);
+                if (nch > 1) prefetch(1);
+            }
+            for (int ci = 0; ci < nch; ++ci) {
+                __syncthreads();
+                if (ci + 1 < nch) commit(ci + 1);
+                if (ci + 2 < nch) prefetch(ci + 2);  // a whole chunk of lead time
+                __syncthreads();
+                if (ci + 1 < nch) a_work(ci + 1);
+            }
+        } else {
+            __syncthreads();
+            if (nch > 0) a_work(0);
+            for (int ci = 0; ci < nch; ++ci) {
+                __syncthreads();
+                // chunk ci's inverses, needed by the B-waves after the next barrier
+                diag_solve_all(ci & 1);
+                t_blocks(ci & 1);
+                __syncthreads();
+                if (ci + 1 < nch) a_work(ci + 1);
+            }
         }
         if (FAM == FAM_SSD && SUMMARY && p.M_out && tile == 0 && wa == 0 && lane == 0)
             p.M_out[int64_t(s) * p.h_v + h] = lam_sum;

@@ -100,6 +100,11 @@ __device__ __forceinline__ void mgemm_tr(const bf16* M, int plane, int stride, c
 // Store an acc tile (rows 4g+r, column c) TRANSPOSED into a 16x16 block:
 // XT[c][4g + r] = v[r] (hi, and lo plane at `plane` when LO); one 8-byte write
 // per lane and plane.
+//
+// The stores stay where they are written (compiler memory barrier): the kernels
+// call this from branches on the wave index, and letting the optimizer sink the
+// stores of several branches into one shared store after the branches has been
+// seen to produce wrong data in LDS.
 template <int SB, bool LO>
 __device__ __forceinline__ void store_tile_tr(bf16* XT, int plane, f32x4 v, int g, int c) {
     if (LO) {
@@ -109,39 +114,36 @@ __device__ __forceinline__ void store_tile_tr(bf16* XT, int plane, f32x4 v, int 
     } else {
         *reinterpret_cast<bf16x4*>(XT + c * SB + 4 * g) = to_bf16(v);
     }
+    asm volatile("" ::: "memory");
 }
 
 // A [CH x DK] token-major K / Q tile prefetched into registers and committed
-// to LDS in kq_pos<DK> order.  Each thread handles 16-byte LDS units (8 columns
-// of one row, per plane); a unit's two 4-column runs are fetched from global
-// memory as two pieces (8 bytes each for bf16, 16 bytes for fp32 inputs, which
-// are split into bf16 hi / lo planes at commit).  Rows t >= n read as zero.
+// to LDS in kq_pos<DK> order.  Each thread handles units of 8 consecutive
+// source columns of one row, fetched from global memory as one 16-byte load
+// (two for fp32 inputs, which are split into bf16 hi / lo planes at commit);
+// the unit's two aligned 4-column runs land at their kq_pos places as two
+// 8-byte LDS writes per plane.  Rows t >= n read as zero.
 template <int CH, int DK, bool F32IO, int NTH>
 struct KQTile {
     static constexpr int UPR = DK / 8;                // units per row
     static constexpr int NU = CH * UPR;               // units per tile
     static constexpr int PER = (NU + NTH - 1) / NTH;  // units per thread
     static constexpr int ES = F32IO ? 4 : 2;          // element bytes in global memory
-    typedef typename std::conditional<F32IO, uint4, uint2>::type Piece;
-    Piece a[PER], b[PER];
-
-    // first column of a unit's first / second run in the source row
-    static __device__ __forceinline__ int run0(int u) { return DK >= 32 ? 32 * (u >> 2) + 4 * (u & 3) : 8 * u; }
-    static __device__ __forceinline__ int run1(int u) { return run0(u) + (DK >= 32 ? 16 : 4); }
+    uint4 a[PER], b[F32IO ? PER : 1];                 // bf16: 8 columns; fp32: columns 0-3 / 4-7
 
     __device__ __forceinline__ void load(const char* base, uint32_t row_bytes, int n, int tid) {
 #pragma unroll
         for (int i = 0; i < PER; ++i) {
             const int idx = tid + i * NTH;
             const int t = idx / UPR, u = idx % UPR;
-            Piece x{}, y{};
+            uint4 x{}, y{};
             if (idx < NU && t < n) {
-                const char* row = base + (uint32_t)t * row_bytes;
-                x = *reinterpret_cast<const Piece*>(row + ES * run0(u));
-                y = *reinterpret_cast<const Piece*>(row + ES * run1(u));
+                const char* src = base + (uint32_t)t * row_bytes + ES * 8 * u;
+                x = *reinterpret_cast<const uint4*>(src);
+                if constexpr (F32IO) y = *reinterpret_cast<const uint4*>(src + 16);
             }
             a[i] = x;
-            b[i] = y;
+            if constexpr (F32IO) b[i] = y;
         }
     }
     // units to LDS rows of stride ds elements (lo plane at dst + pofs for fp32 io)
@@ -151,14 +153,18 @@ struct KQTile {
             const int idx = tid + i * NTH;
             if (NU % NTH != 0 && idx >= NU) continue;
             const int t = idx / UPR, u = idx % UPR;
-            bf16* d = dst + t * ds + 8 * u;
+            bf16* d = dst + t * ds;
+            const int p0 = kq_pos<DK>(8 * u), p1 = kq_pos<DK>(8 * u + 4);
             if constexpr (!F32IO) {
-                *reinterpret_cast<uint4*>(d) = uint4{a[i].x, a[i].y, b[i].x, b[i].y};
+                *reinterpret_cast<uint2*>(d + p0) = uint2{a[i].x, a[i].y};
+                *reinterpret_cast<uint2*>(d + p1) = uint2{a[i].z, a[i].w};
             } else {
                 const Split4 sa = split4(__builtin_bit_cast(f32x4, a[i]));
                 const Split4 sb = split4(__builtin_bit_cast(f32x4, b[i]));
-                *reinterpret_cast<bf16x8*>(d) = __builtin_shufflevector(sa.hi, sb.hi, 0, 1, 2, 3, 4, 5, 6, 7);
-                *reinterpret_cast<bf16x8*>(d + pofs) = __builtin_shufflevector(sa.lo, sb.lo, 0, 1, 2, 3, 4, 5, 6, 7);
+                *reinterpret_cast<bf16x4*>(d + p0) = sa.hi;
+                *reinterpret_cast<bf16x4*>(d + p1) = sb.hi;
+                *reinterpret_cast<bf16x4*>(d + pofs + p0) = sa.lo;
+                *reinterpret_cast<bf16x4*>(d + pofs + p1) = sb.lo;
             }
         }
     }
