@@ -131,7 +131,7 @@ __device__ __forceinline__ constexpr int low_mt(int j) {
 }
 
 template <int FAM, int DK, int CH, bool F32IO, int NB, bool SUMMARY>
-__global__ __launch_bounds__(64 * (NB + NA)) void chunk_kernel(ScanArgs p) {
+__global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(ScanArgs p) {
     using Ly = ChunkLds<FAM, DK, CH, F32IO, NB, SUMMARY>;
     constexpr int NTC = CH / 16, NTK = DK / 16;
     constexpr int SK = Ly::SK, SV = Ly::SV, SB = Ly::SB, BLK = Ly::BLK, SLD = Ly::SLD;
@@ -822,6 +822,11 @@ hipError_t launch_chunk_s(const ScanArgs& a, hipStream_t st) {
         case 1: return launch_chunk_nb<FAM, DK, CH, F32IO, 1, SUMMARY>(a, st);
         case 2: return launch_chunk_nb<FAM, DK, CH, F32IO, 2, SUMMARY>(a, st);
         case 4: return launch_chunk_nb<FAM, DK, CH, F32IO, 4, SUMMARY>(a, st);
+        case 8:
+            // a whole 128-row transition per workgroup: the state-independent work of
+            // a chunk is shared by eight state waves
+            if constexpr (SUMMARY && DK == 128 && !F32IO) return launch_chunk_nb<FAM, DK, CH, F32IO, 8, SUMMARY>(a, st);
+            return hipErrorInvalidValue;
     }
     return hipErrorInvalidValue;
 }
@@ -843,6 +848,7 @@ size_t chunk_lds_t(int nb, bool summary) {
         case 5: return ChunkLds<FAM, DK, CH, F32IO, 2, true>::BYTES;
         case 8: return ChunkLds<FAM, DK, CH, F32IO, 4, false>::BYTES;
         case 9: return ChunkLds<FAM, DK, CH, F32IO, 4, true>::BYTES;
+        case 17: return (DK == 128 && !F32IO) ? ChunkLds<FAM, DK, CH, F32IO, 8, true>::BYTES : 0;
     }
     return 0;
 }

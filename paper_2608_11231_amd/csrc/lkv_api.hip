@@ -48,9 +48,10 @@ int env_int(const char* name, int dflt) {
 int pick_nw(int fam, int dk, int chunk, bool f32io, int64_t pairs, int rows, int rows2, bool summary) {
     int forced = env_int("LKV_SCAN_NB", 0);
     int fallback = 0;
-    for (int nb = 4; nb >= 1; nb >>= 1) {
+    for (int nb = summary ? 8 : 4; nb >= 1; nb >>= 1) {
         if (rows % (16 * nb) || (rows2 && rows2 % (16 * nb))) continue;
-        if (scan_lds_bytes(fam, dk, chunk, f32io, nb, summary) > 160 * 1024) continue;
+        const size_t lds = scan_lds_bytes(fam, dk, chunk, f32io, nb, summary);
+        if (lds == 0 || lds > 160 * 1024) continue;
         if (forced) {
             if (nb == forced) return nb;
             continue;
