@@ -130,9 +130,10 @@ __device__ __forceinline__ constexpr int low_mt(int j) {
     return mt;
 }
 
-template <int FAM, int DK, int CH, bool F32IO, int NB, bool SUMMARY>
+template <int FAM, int DK, int CH, bool F32IO, int NB, bool SUMMARY, int RT = 1>
 __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(ScanArgs p) {
-    using Ly = ChunkLds<FAM, DK, CH, F32IO, NB, SUMMARY>;
+    static_assert(RT == 1 || SUMMARY, "several row tiles per wave: block summaries only");
+    using Ly = ChunkLds<FAM, DK, CH, F32IO, NB * RT, SUMMARY>;
     constexpr int NTC = CH / 16, NTK = DK / 16;
     constexpr int SK = Ly::SK, SV = Ly::SV, SB = Ly::SB, BLK = Ly::BLK, SLD = Ly::SLD;
     constexpr int NOFF = Ly::NOFF, NPB = Ly::NPB;
@@ -155,8 +156,7 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
     const int h = (u / tiles) % p.h_v;
     const int s = u / (tiles * p.h_v);
     const bool mtile = tile >= p.tiles_b;
-    const int row0 = (mtile ? tile - p.tiles_b : tile) * 16 * NB;
-    const int my_row = row0 + 16 * w + c16;  // B-waves: this lane's state row
+    const int row0 = (mtile ? tile - p.tiles_b : tile) * 16 * NB * RT;  // first state row of the tile
     const int hq = h / (p.h_v / p.h_qk);
     int64_t t0 = p.cu[s], t1 = p.cu[s + 1];
     t0 = t0 < 0 ? 0 : (t0 > p.n_tok ? p.n_tok : t0);
@@ -276,27 +276,34 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
     // each role's registers are allocated on its own: the B-waves' state and the
     // A-waves' prefetch registers never have to be live at the same time.
     if (is_b) {
-        // ---- the state (acc layout: tile nt holds S[my_row][16nt + 4g + r])
-        f32x4 S[NTK];
+        // ---- the state: RT row tiles per wave, tile rt covering rows row_of(rt);
+        // acc layout: S[rt][nt] holds S[row][16nt + 4g + r]
+        auto row_of = [&](int rt) { return row0 + 16 * (RT * w + rt) + c16; };
+        f32x4 S[RT][NTK];
 #pragma unroll
-        for (int nt = 0; nt < NTK; ++nt) {
-            if (!SUMMARY && p.S_init) {
-                S[nt] = *reinterpret_cast<const f32x4*>(
-                    p.S_init + ((int64_t(s) * p.h_v + h) * p.dv + my_row) * DK + 16 * nt + 4 * g);
-            } else {
-#pragma unroll
-                for (int r = 0; r < 4; ++r) S[nt][r] = (mtile && my_row == 16 * nt + 4 * g + r) ? 1.f : 0.f;
-            }
-        }
-        // bf16 hi / lo parts of the state, refreshed after every state update
-        bf16x4 Sh[NTK], Sl[NTK];
-        auto split_state = [&]() {
+        for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
             for (int nt = 0; nt < NTK; ++nt) {
-                const Split4 sp = split4(S[nt]);
-                Sh[nt] = sp.hi;
-                Sl[nt] = sp.lo;
+                const int row = row_of(rt);
+                if (!SUMMARY && p.S_init) {
+                    S[rt][nt] = *reinterpret_cast<const f32x4*>(
+                        p.S_init + ((int64_t(s) * p.h_v + h) * p.dv + row) * DK + 16 * nt + 4 * g);
+                } else {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) S[rt][nt][r] = (mtile && row == 16 * nt + 4 * g + r) ? 1.f : 0.f;
+                }
             }
+        // bf16 hi / lo parts of the state, refreshed after every state update
+        bf16x4 Sh[RT][NTK], Sl[RT][NTK];
+        auto split_state = [&]() {
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                for (int nt = 0; nt < NTK; ++nt) {
+                    const Split4 sp = split4(S[rt][nt]);
+                    Sh[rt][nt] = sp.hi;
+                    Sl[rt][nt] = sp.lo;
+                }
         };
         split_state();
         __syncthreads();  // prologue: chunk 0 staged by the A-waves
@@ -306,18 +313,21 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
             const int n = (int)((t1 - c0) < CH ? (t1 - c0) : CH);
             __syncthreads();
             // ================= phase I: K S^T and the delta-rule right-hand side
-            f32x4 X[NTC];
+            f32x4 X[RT][NTC];
             {
                 const bf16* Kb = sK(b);
                 const float* G = sG(b);
 #pragma unroll
-                for (int mt = 0; mt < NTC; ++mt) {
-                    X[mt] = zero4();
-                    if (load_v) {
-                        X[mt] = to_f32(lds4_tr(sV(b), SV, 16 * mt, 16 * w, g, c16));
-                        if (F32IO) X[mt] += to_f32(lds4_tr(sV(b) + VPL, SV, 16 * mt, 16 * w, g, c16));
+                for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                    for (int mt = 0; mt < NTC; ++mt) {
+                        X[rt][mt] = zero4();
+                        if (load_v) {
+                            const int col = 16 * (RT * w + rt);
+                            X[rt][mt] = to_f32(lds4_tr(sV(b), SV, 16 * mt, col, g, c16));
+                            if (F32IO) X[rt][mt] += to_f32(lds4_tr(sV(b) + VPL, SV, 16 * mt, col, g, c16));
+                        }
                     }
-                }
                 if (with_out) {
                     // this chunk's output blocks P, shared by the B-waves (read after the barrier)
                     using NS = integral_constant<int, NB>;
@@ -331,17 +341,25 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                 }
                 if (FAM == FAM_GDN) {
                     // K S^T for all token tiles at once (interleaved chains, hi and lo passes apart)
-                    f32x4 kh[NTC], kl[NTC];
+                    f32x4 kh[RT][NTC], kl[RT][NTC];
 #pragma unroll
-                    for (int mt = 0; mt < NTC; ++mt) kh[mt] = kl[mt] = zero4();
-                    mgemm_rows<NTC, F32IO, true>(Kb + c16 * SK, 16 * SK, KPL, Sh, Sl, NTK, g, kh, kl);
+                    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                        for (int mt = 0; mt < NTC; ++mt) kh[rt][mt] = kl[rt][mt] = zero4();
+                    if constexpr (RT == 1)
+                        mgemm_rows<NTC, F32IO, true>(Kb + c16 * SK, 16 * SK, KPL, Sh[0], Sl[0], NTK, g, kh[0], kl[0]);
+                    else
+                        mgemm_rows_rt<NTC, RT, NTK, F32IO, true>(Kb + c16 * SK, 16 * SK, KPL, Sh, Sl, g, kh, kl);
 #pragma unroll
                     for (int mt = 0; mt < NTC; ++mt) {
                         const f32x4 bt = lds4f(G + 2 * CH + 16 * mt + 4 * g);
                         const f32x4 be = lds4f(G + CH + 16 * mt + 4 * g);
-                        const f32x4 ks = kh[mt] + kl[mt];
 #pragma unroll
-                        for (int r = 0; r < 4; ++r) X[mt][r] = be[r] * (X[mt][r] - bt[r] * ks[r]);
+                        for (int rt = 0; rt < RT; ++rt) {
+                            const f32x4 ks = kh[rt][mt] + kl[rt][mt];
+#pragma unroll
+                            for (int r = 0; r < 4; ++r) X[rt][mt][r] = be[r] * (X[rt][mt][r] - bt[r] * ks[r]);
+                        }
                     }
                 }
             }
@@ -350,10 +368,10 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
             {
                 const bf16* Kb = sK(b);
                 const float* G = sG(b);
-                // Outputs are formed transposed, O^T = S Q^T + U^T P^T: tile mt holds
-                // O[16mt + c16][this wave's rows 4g..4g+3], so each lane stores 4
-                // consecutive state rows of one token.  S Q^T does not depend on U and
-                // is issued first, alongside the substitution chain.
+                // Outputs (RT == 1 only) are formed transposed, O^T = S Q^T + U^T P^T:
+                // tile mt holds O[16mt + c16][this wave's rows 4g..4g+3], so each lane
+                // stores 4 consecutive state rows of one token.  S Q^T does not depend
+                // on U and is issued first, alongside the substitution chain.
                 f32x4 OT[NTC];
                 if (with_out) {
                     const bf16* Qb = sQ(b);
@@ -363,10 +381,10 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
 #pragma unroll
                         for (int mt = 0; mt < NTC; ++mt) {
                             const bf16* qr = Qb + (16 * mt + c16) * SK + 4 * g;
-                            OT[mt] = mma16(Sh[0], lds4(qr), OT[mt]);
+                            OT[mt] = mma16(Sh[0][0], lds4(qr), OT[mt]);
                             if (F32IO) {
-                                OT[mt] = mma16(Sl[0], lds4(qr), OT[mt]);
-                                OT[mt] = mma16(Sh[0], lds4(qr + KPL), OT[mt]);
+                                OT[mt] = mma16(Sl[0][0], lds4(qr), OT[mt]);
+                                OT[mt] = mma16(Sh[0][0], lds4(qr + KPL), OT[mt]);
                             }
                         }
                     } else {
@@ -385,16 +403,16 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                         for (int kp = 0; kp < NKP; ++kp)
 #pragma unroll
                             for (int mt = 0; mt < NTC; ++mt) {
-                                OT[mt] = mma32(Sh[2 * kp], Sh[2 * kp + 1], qh[kp][mt], OT[mt]);
+                                OT[mt] = mma32(Sh[0][2 * kp], Sh[0][2 * kp + 1], qh[kp][mt], OT[mt]);
                                 if constexpr (F32IO) {
-                                    OT[mt] = mma32(Sl[2 * kp], Sl[2 * kp + 1], qh[kp][mt], OT[mt]);
-                                    OT[mt] = mma32(Sh[2 * kp], Sh[2 * kp + 1], ql[kp][mt], OT[mt]);
+                                    OT[mt] = mma32(Sl[0][2 * kp], Sl[0][2 * kp + 1], qh[kp][mt], OT[mt]);
+                                    OT[mt] = mma32(Sh[0][2 * kp], Sh[0][2 * kp + 1], ql[kp][mt], OT[mt]);
                                 }
                             }
                     }
                 }
-                f32x4 U[NTC];
-                bf16x4 Uh[NTC], Ul[NTC];
+                f32x4 U[RT][NTC];
+                bf16x4 Uh[RT][NTC], Ul[RT][NTC];
                 // output blocks P (transposed fragments), independent of U: requested early
                 constexpr int PPL = (!SUMMARY && F32IO) ? 2 : 1;
                 bf16x4 Pf[PPL][SUMMARY ? 1 : NPB];
@@ -410,9 +428,9 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                     //   U_A = T_A X_A,  U_B = T_B (X_B - L_BA U_A),
                     // with T_A = [[N_0, 0], [T_10, N_1]], T_B = [[N_2, 0], [T_32, N_3]] (the
                     // 16x16 diagonal inverses N and T_10 = -N_1 L_10 N_0, T_32 = -N_3 L_32 N_2
-                    // come from the A-waves).  Three dependent stages; the hi*hi and the
-                    // correction passes accumulate apart.  All fragments are requested
-                    // before the first product.
+                    // come from the A-waves).  Three dependent stages, the row tiles
+                    // interleaved; the hi*hi and the correction passes accumulate apart.
+                    // All fragments are requested before the first product.
                     const bf16* LT = sLT(b);
                     const bf16* NT = sNT(b);
                     bf16x4 Nh[NTC], Nl[NTC];
@@ -421,18 +439,21 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                         Nh[mt] = lds4_tr(NT + mt * BLK, SB, 0, 0, g, c16);
                         Nl[mt] = lds4_tr(NT + (NTC + mt) * BLK, SB, 0, 0, g, c16);
                     }
-                    auto split_u = [&](int mt, f32x4 v) {
-                        U[mt] = v;
+                    auto split_u = [&](int rt, int mt, f32x4 v) {
+                        U[rt][mt] = v;
                         const Split4 us = split4(v);
-                        Uh[mt] = us.hi;
-                        Ul[mt] = us.lo;
+                        Uh[rt][mt] = us.hi;
+                        Ul[rt][mt] = us.lo;
                     };
                     if constexpr (NTC == 1) {
-                        const Split4 xs = split4(X[0]);
-                        const f32x4 u0 = mma16(Nh[0], xs.hi, zero4());
-                        f32x4 u1 = mma16(Nh[0], xs.lo, zero4());
-                        u1 = mma16(Nl[0], xs.hi, u1);
-                        split_u(0, u0 + u1);
+#pragma unroll
+                        for (int rt = 0; rt < RT; ++rt) {
+                            const Split4 xs = split4(X[rt][0]);
+                            const f32x4 u0 = mma16(Nh[0], xs.hi, zero4());
+                            f32x4 u1 = mma16(Nh[0], xs.lo, zero4());
+                            u1 = mma16(Nl[0], xs.hi, u1);
+                            split_u(rt, 0, u0 + u1);
+                        }
                     } else {
                         static_assert(NTC == 4, "chunk of 16 or 64 tokens");
                         const bf16* TT = sTT(b);
@@ -448,40 +469,54 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                             Ll[j] = lds4_tr(LT + (NOFF + 1 + j) * BLK, SB, 0, 0, g, c16);
                         }
                         // stage 1: U_0 = N_0 X_0, U_1 = T_10 X_0 + N_1 X_1
-                        const Split4 x0 = split4(X[0]), x1 = split4(X[1]);
-                        const f32x4 u0h = mma16(Nh[0], x0.hi, zero4());
-                        const f32x4 u1h = mma32(t10h, Nh[1], x0.hi, x1.hi, zero4());
-                        f32x4 u0l = mma16(Nh[0], x0.lo, zero4());
-                        f32x4 u1l = mma32(t10h, Nh[1], x0.lo, x1.lo, zero4());
-                        u0l = mma16(Nl[0], x0.hi, u0l);
-                        u1l = mma32(t10l, Nl[1], x0.hi, x1.hi, u1l);
-                        split_u(0, u0h + u0l);
-                        split_u(1, u1h + u1l);
+#pragma unroll
+                        for (int rt = 0; rt < RT; ++rt) {
+                            const Split4 x0 = split4(X[rt][0]), x1 = split4(X[rt][1]);
+                            const f32x4 u0h = mma16(Nh[0], x0.hi, zero4());
+                            const f32x4 u1h = mma32(t10h, Nh[1], x0.hi, x1.hi, zero4());
+                            f32x4 u0l = mma16(Nh[0], x0.lo, zero4());
+                            f32x4 u1l = mma32(t10h, Nh[1], x0.lo, x1.lo, zero4());
+                            u0l = mma16(Nl[0], x0.hi, u0l);
+                            u1l = mma32(t10l, Nl[1], x0.hi, x1.hi, u1l);
+                            split_u(rt, 0, u0h + u0l);
+                            split_u(rt, 1, u1h + u1l);
+                        }
                         // stage 2: R_2 = X_2 - L_20 U_0 - L_21 U_1, R_3 = X_3 - L_30 U_0 - L_31 U_1
-                        const f32x4 r2h = mma32(Lh[0], Lh[1], Uh[0], Uh[1], X[2]);
-                        const f32x4 r3h = mma32(Lh[2], Lh[3], Uh[0], Uh[1], X[3]);
-                        f32x4 r2l = mma32(Lh[0], Lh[1], Ul[0], Ul[1], zero4());
-                        f32x4 r3l = mma32(Lh[2], Lh[3], Ul[0], Ul[1], zero4());
-                        r2l = mma32(Ll[0], Ll[1], Uh[0], Uh[1], r2l);
-                        r3l = mma32(Ll[2], Ll[3], Uh[0], Uh[1], r3l);
-                        const Split4 x2 = split4(r2h + r2l), x3 = split4(r3h + r3l);
+                        Split4 x2[RT], x3[RT];
+#pragma unroll
+                        for (int rt = 0; rt < RT; ++rt) {
+                            const f32x4 r2h = mma32(Lh[0], Lh[1], Uh[rt][0], Uh[rt][1], X[rt][2]);
+                            const f32x4 r3h = mma32(Lh[2], Lh[3], Uh[rt][0], Uh[rt][1], X[rt][3]);
+                            f32x4 r2l = mma32(Lh[0], Lh[1], Ul[rt][0], Ul[rt][1], zero4());
+                            f32x4 r3l = mma32(Lh[2], Lh[3], Ul[rt][0], Ul[rt][1], zero4());
+                            r2l = mma32(Ll[0], Ll[1], Uh[rt][0], Uh[rt][1], r2l);
+                            r3l = mma32(Ll[2], Ll[3], Uh[rt][0], Uh[rt][1], r3l);
+                            x2[rt] = split4(r2h + r2l);
+                            x3[rt] = split4(r3h + r3l);
+                        }
                         // stage 3: U_2 = N_2 R_2, U_3 = T_32 R_2 + N_3 R_3
-                        const f32x4 u2h = mma16(Nh[2], x2.hi, zero4());
-                        const f32x4 u3h = mma32(t32h, Nh[3], x2.hi, x3.hi, zero4());
-                        f32x4 u2l = mma16(Nh[2], x2.lo, zero4());
-                        f32x4 u3l = mma32(t32h, Nh[3], x2.lo, x3.lo, zero4());
-                        u2l = mma16(Nl[2], x2.hi, u2l);
-                        u3l = mma32(t32l, Nl[3], x2.hi, x3.hi, u3l);
-                        split_u(2, u2h + u2l);
-                        split_u(3, u3h + u3l);
+#pragma unroll
+                        for (int rt = 0; rt < RT; ++rt) {
+                            const f32x4 u2h = mma16(Nh[2], x2[rt].hi, zero4());
+                            const f32x4 u3h = mma32(t32h, Nh[3], x2[rt].hi, x3[rt].hi, zero4());
+                            f32x4 u2l = mma16(Nh[2], x2[rt].lo, zero4());
+                            f32x4 u3l = mma32(t32h, Nh[3], x2[rt].lo, x3[rt].lo, zero4());
+                            u2l = mma16(Nl[2], x2[rt].hi, u2l);
+                            u3l = mma32(t32l, Nl[3], x2[rt].hi, x3[rt].hi, u3l);
+                            split_u(rt, 2, u2h + u2l);
+                            split_u(rt, 3, u3h + u3l);
+                        }
                     }
                 } else {
 #pragma unroll
-                    for (int mt = 0; mt < NTC; ++mt) {
-                        U[mt] = X[mt];
-                        Uh[mt] = lds4_tr(sV(b), SV, 16 * mt, 16 * w, g, c16);
-                        Ul[mt] = F32IO ? lds4_tr(sV(b) + VPL, SV, 16 * mt, 16 * w, g, c16) : zero_bf16x4();
-                    }
+                    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                        for (int mt = 0; mt < NTC; ++mt) {
+                            const int col = 16 * (RT * w + rt);
+                            U[rt][mt] = X[rt][mt];
+                            Uh[rt][mt] = lds4_tr(sV(b), SV, 16 * mt, col, g, c16);
+                            Ul[rt][mt] = F32IO ? lds4_tr(sV(b) + VPL, SV, 16 * mt, col, g, c16) : zero_bf16x4();
+                        }
                 }
                 if (with_out) {
                     const float coef = (FAM == FAM_GDN) ? p.scale : 1.f;
@@ -490,10 +525,10 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                     // + U^T P^T: tile mt contracts over token blocks 0..mt, pairs of blocks per MFMA
                     if constexpr (NTC == 1) {
                         const bf16x4 x = Pf[0][0];
-                        OT[0] = mma16(Uh[0], x, OT[0]);
+                        OT[0] = mma16(Uh[0][0], x, OT[0]);
                         if (F32IO) {
-                            OT[0] = mma16(Ul[0], x, OT[0]);
-                            OT[0] = mma16(Uh[0], Pf[PPL - 1][0], OT[0]);
+                            OT[0] = mma16(Ul[0][0], x, OT[0]);
+                            OT[0] = mma16(Uh[0][0], Pf[PPL - 1][0], OT[0]);
                         }
                     } else {
 #pragma unroll
@@ -505,14 +540,14 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                                 const int j0 = low_index(mt, kp);
                                 const bf16x4 x0 = Pf[0][j0];
                                 const bf16x4 x1 = two ? Pf[0][j0 + 1] : zero_bf16x4();
-                                const bf16x4 u1h = two ? Uh[kp + 1] : zero_bf16x4();
-                                OT[mt] = mma32(Uh[kp], u1h, x0, x1, OT[mt]);
+                                const bf16x4 u1h = two ? Uh[0][kp + 1] : zero_bf16x4();
+                                OT[mt] = mma32(Uh[0][kp], u1h, x0, x1, OT[mt]);
                                 if (F32IO) {
-                                    const bf16x4 u1l = two ? Ul[kp + 1] : zero_bf16x4();
-                                    OT[mt] = mma32(Ul[kp], u1l, x0, x1, OT[mt]);
+                                    const bf16x4 u1l = two ? Ul[0][kp + 1] : zero_bf16x4();
+                                    OT[mt] = mma32(Ul[0][kp], u1l, x0, x1, OT[mt]);
                                     const bf16x4 y0 = Pf[PPL - 1][j0];
                                     const bf16x4 y1 = two ? Pf[PPL - 1][j0 + 1] : zero_bf16x4();
-                                    OT[mt] = mma32(Uh[kp], u1h, y0, y1, OT[mt]);
+                                    OT[mt] = mma32(Uh[0][kp], u1h, y0, y1, OT[mt]);
                                 }
                             }
                         }
@@ -529,19 +564,27 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                         }
                     }
                 }
-                // S <- b_C S + K^T diag(w) U   (all dk tiles interleaved)
-                bf16x4 Wh[NTC], Wl[NTC];
+                // S <- b_C S + K^T diag(w) U   (all dk tiles and row tiles interleaved)
+                bf16x4 Wh[RT][NTC], Wl[RT][NTC];
 #pragma unroll
                 for (int mt = 0; mt < NTC; ++mt) {
                     const f32x4 wt = lds4f(G + 3 * CH + 16 * mt + 4 * g);
-                    const Split4 sp = split4(wt * U[mt]);
-                    Wh[mt] = sp.hi;
-                    Wl[mt] = sp.lo;
+#pragma unroll
+                    for (int rt = 0; rt < RT; ++rt) {
+                        const Split4 sp = split4(wt * U[rt][mt]);
+                        Wh[rt][mt] = sp.hi;
+                        Wl[rt][mt] = sp.lo;
+                    }
                 }
                 const float bC = G[5 * CH];
 #pragma unroll
-                for (int nt = 0; nt < NTK; ++nt) S[nt] = bC * S[nt];
-                mgemm_tr<DK, NTK, F32IO, true>(Kb, KPL, SK, Wh, Wl, NTC, g, c16, S);
+                for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                    for (int nt = 0; nt < NTK; ++nt) S[rt][nt] = bC * S[rt][nt];
+                if constexpr (RT == 1)
+                    mgemm_tr<DK, NTK, F32IO, true>(Kb, KPL, SK, Wh[0], Wl[0], NTC, g, c16, S[0]);
+                else
+                    mgemm_tr_rt<DK, NTK, RT, NTC, F32IO, true>(Kb, KPL, SK, Wh, Wl, g, c16, S);
                 split_state();  // for the next chunk, ahead of its barrier
             }
         }
@@ -549,9 +592,11 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
         if (dst) {
             const int rows = mtile ? DK : p.dv;
 #pragma unroll
-            for (int nt = 0; nt < NTK; ++nt)
-                *reinterpret_cast<f32x4*>(dst + ((int64_t(s) * p.h_v + h) * rows + my_row) * DK + 16 * nt + 4 * g) =
-                    S[nt];
+            for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                for (int nt = 0; nt < NTK; ++nt)
+                    *reinterpret_cast<f32x4*>(dst + ((int64_t(s) * p.h_v + h) * rows + row_of(rt)) * DK + 16 * nt +
+                                              4 * g) = S[rt][nt];
         }
     } else {
         // ---- A-waves: HBM -> register prefetch and register -> LDS commit of a chunk
@@ -560,7 +605,7 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
         constexpr int NSTG = (FAM == FAM_GDN) ? NA - 1 : NA;
         const bool stager = wa < NSTG;
         KQTile<CH, DK, F32IO, 64 * NSTG> pk, pq;
-        TileRegs<CH, 16 * NB, F32IO, 64 * NSTG> pv;
+        TileRegs<CH, 16 * NB * RT, F32IO, 64 * NSTG> pv;
         uint32_t pg = 0u, pb = 0u;  // gates stay raw bits until commit (no early wait on the loads)
         float lam_sum = 0.f;
         constexpr int ES = F32IO ? 4 : 2;
@@ -805,10 +850,10 @@ hipError_t launch_scan_gdn(int dk, int chunk, bool f32io, const ScanArgs& a, hip
 hipError_t launch_scan_ssd(int dk, int chunk, bool f32io, const ScanArgs& a, hipStream_t st);
 size_t scan_lds_bytes(int fam, int dk, int chunk, bool f32io, int nb, bool summary);
 
-template <int FAM, int DK, int CH, bool F32IO, int NB, bool SUMMARY>
+template <int FAM, int DK, int CH, bool F32IO, int NB, bool SUMMARY, int RT = 1>
 hipError_t launch_chunk_nb(const ScanArgs& a, hipStream_t st) {
-    const size_t lds = ChunkLds<FAM, DK, CH, F32IO, NB, SUMMARY>::BYTES;
-    auto kern = chunk_kernel<FAM, DK, CH, F32IO, NB, SUMMARY>;
+    const size_t lds = ChunkLds<FAM, DK, CH, F32IO, NB * RT, SUMMARY>::BYTES;
+    auto kern = chunk_kernel<FAM, DK, CH, F32IO, NB, SUMMARY, RT>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
@@ -824,8 +869,10 @@ hipError_t launch_chunk_s(const ScanArgs& a, hipStream_t st) {
         case 4: return launch_chunk_nb<FAM, DK, CH, F32IO, 4, SUMMARY>(a, st);
         case 8:
             // a whole 128-row transition per workgroup: the state-independent work of
-            // a chunk is shared by eight state waves
-            if constexpr (SUMMARY && DK == 128 && !F32IO) return launch_chunk_nb<FAM, DK, CH, F32IO, 8, SUMMARY>(a, st);
+            // a chunk is shared by four state waves of two row tiles each, which
+            // also share every K fragment they read
+            if constexpr (SUMMARY && DK == 128 && CH == 64 && !F32IO)
+                return launch_chunk_nb<FAM, DK, CH, F32IO, 4, SUMMARY, 2>(a, st);
             return hipErrorInvalidValue;
     }
     return hipErrorInvalidValue;
@@ -848,7 +895,7 @@ size_t chunk_lds_t(int nb, bool summary) {
         case 5: return ChunkLds<FAM, DK, CH, F32IO, 2, true>::BYTES;
         case 8: return ChunkLds<FAM, DK, CH, F32IO, 4, false>::BYTES;
         case 9: return ChunkLds<FAM, DK, CH, F32IO, 4, true>::BYTES;
-        case 17: return (DK == 128 && !F32IO) ? ChunkLds<FAM, DK, CH, F32IO, 8, true>::BYTES : 0;
+        case 17: return (DK == 128 && CH == 64 && !F32IO) ? ChunkLds<FAM, DK, CH, F32IO, 8, true>::BYTES : 0;
     }
     return 0;
 }

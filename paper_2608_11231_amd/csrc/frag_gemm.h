@@ -57,6 +57,66 @@ __device__ __forceinline__ void mgemm_rows(const bf16* a0, int mstep, int plane,
     }
 }
 
+// mgemm_rows for RT independent right-hand sides B_rt (the state row tiles of
+// one wave) sharing every A fragment: acc_h[rt][m] += A_m x B_rt (hi passes),
+// acc_l[rt][m] += lo passes.  nk = NTK 16-slices (even, at least 2).
+template <int NM, int RT, int NTK, bool ALO, bool BLO>
+__device__ __forceinline__ void mgemm_rows_rt(const bf16* a0, int mstep, int plane, const bf16x4 (&bh)[RT][NTK],
+                                              const bf16x4 (&bl)[RT][NTK], int g, f32x4 (&acc_h)[RT][NM],
+                                              f32x4 (&acc_l)[RT][NM]) {
+    static_assert(NTK % 2 == 0, "32-wide slices");
+    constexpr int NP = NTK / 2;
+#pragma unroll
+    for (int kp = 0; kp < NP; ++kp) {
+        bf16x8 xh[NM], xl[ALO ? NM : 1];
+#pragma unroll
+        for (int m = 0; m < NM; ++m) {
+            const bf16* ar = a0 + m * mstep + 32 * kp + 8 * g;
+            xh[m] = lds8(ar);
+            if constexpr (ALO) xl[m] = lds8(ar + plane);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int m = 0; m < NM; ++m)
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) {
+                acc_h[rt][m] = mma32(xh[m], bh[rt][2 * kp], bh[rt][2 * kp + 1], acc_h[rt][m]);
+                if (BLO) acc_l[rt][m] = mma32(xh[m], bl[rt][2 * kp], bl[rt][2 * kp + 1], acc_l[rt][m]);
+                if constexpr (ALO) acc_l[rt][m] = mma32(xl[m], bh[rt][2 * kp], bh[rt][2 * kp + 1], acc_l[rt][m]);
+            }
+    }
+}
+
+// mgemm_tr for RT right-hand sides sharing every transposed A fragment:
+// acc[rt][n] += M^T(columns 16n..) x B_rt, nk = NK token 16-slices (even).
+template <int DK, int NN, int RT, int NK, bool ALO, bool BLO>
+__device__ __forceinline__ void mgemm_tr_rt(const bf16* M, int plane, int stride, const bf16x4 (&bh)[RT][NK],
+                                            const bf16x4 (&bl)[RT][NK], int g, int c, f32x4 (&acc)[RT][NN]) {
+    static_assert(NK % 2 == 0, "32-wide slices");
+#pragma unroll
+    for (int kg = 0; kg < NK; kg += 2) {
+        bf16x4 x0[NN], x1[NN], y0[ALO ? NN : 1], y1[ALO ? NN : 1];
+#pragma unroll
+        for (int n = 0; n < NN; ++n) {
+            x0[n] = lds4_tr_kq<DK>(M, stride, 16 * kg, 16 * n, g, c);
+            x1[n] = lds4_tr_kq<DK>(M, stride, 16 * kg + 16, 16 * n, g, c);
+            if constexpr (ALO) {
+                y0[n] = lds4_tr_kq<DK>(M + plane, stride, 16 * kg, 16 * n, g, c);
+                y1[n] = lds4_tr_kq<DK>(M + plane, stride, 16 * kg + 16, 16 * n, g, c);
+            }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int n = 0; n < NN; ++n)
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) {
+                acc[rt][n] = mma32(x0[n], x1[n], bh[rt][kg], bh[rt][kg + 1], acc[rt][n]);
+                if (BLO) acc[rt][n] = mma32(x0[n], x1[n], bl[rt][kg], bl[rt][kg + 1], acc[rt][n]);
+                if constexpr (ALO) acc[rt][n] = mma32(y0[n], y1[n], bh[rt][kg], bh[rt][kg + 1], acc[rt][n]);
+            }
+    }
+}
+
 // acc[n] += M^T(columns 16n..16n+15) x B for NN tiles, the A fragments read
 // transposed from a token-major K / Q tile M in kq_pos<DK> order (rows =
 // contraction, hi plane; lo plane at + plane).  All passes accumulate into acc[n].
