@@ -250,8 +250,15 @@ def main():
     table = rocprof_summary.read_traffic(os.path.join(ROOT, "profiles", f"{w.name}_hbm_traffic.txt"))
     if table:
         fam = w.layer.family
-        pick = {"scan": lambda n: n.startswith(f"lkv::chunk_kernel<{fam},") and n.endswith(",false>"),
-                "fold": lambda n: n.startswith(f"lkv::chunk_kernel<{fam},") and n.endswith(",true>"),
+        def chunk_mode(n):
+            # lkv::chunk_kernel<FAM,DK,CH,F32IO,NB,SUMMARY,RT>: family and summary flag
+            if not n.startswith("lkv::chunk_kernel<"):
+                return None
+            args = n[len("lkv::chunk_kernel<"):].rstrip(">").split(",")
+            return (int(args[0]), args[5] == "true") if len(args) >= 6 else None
+
+        pick = {"scan": lambda n: chunk_mode(n) == (fam, False),
+                "fold": lambda n: chunk_mode(n) == (fam, True),
                 "compose": lambda n: "compose" in n,
                 "init_single": lambda n: "init_single" in n}
         for op, pred in pick.items():
