@@ -17,6 +17,9 @@ durations come from HIP events on the stream the library launches on, inside
 the timed region; ``roofline`` is given for the kernel that takes the most time
 and ``roofline_by_kernel`` for all four.  ``cpu_baseline`` times the CPU oracle
 on a bounded sample of the same workload and scales it to the whole step.
+``decode_step`` times, after the step and outside it, the decode call that
+follows the prefill (one token per request) on the workload's final states and
+on a 256-request batch.
 """
 import argparse
 import json
@@ -103,6 +106,48 @@ def roofline(name, work, ms):
                 algorithmic_flops=work["flops"], algorithmic_bytes=work["bytes"])
 
 
+# ---------------------------------------------------------------- decode step
+def decode_bench(w, S_final, steps: int, batches=(None, 256)):
+    """Time the decode step (one token per request) of the workload's layer: on the
+    workload's own final states and on a larger decode batch.  Algorithmic bytes =
+    every state element read and written once (fp32) plus the token's q/k/v,
+    gates and outputs; the bound is HBM."""
+    import torch
+    from paper_2608_11231_amd import gpu_io
+    from paper_2608_11231_amd import inputs as I
+    L = w.layer
+    io = 2 if L.io_dtype == "bf16" else 4
+    gb = 2 if (L.gate_dtype == "bf16" and L.family == I.GDN) else 4
+    n_gates = 2 if L.family == I.GDN else 1
+    res = {}
+    for n_req in batches:
+        n_req = w.n_req if n_req is None else n_req
+        dw = I.build_workload("decode", L, [[] for _ in range(n_req)], [1] * n_req, I.GateLaw(), 77,
+                              scale=w.scale)
+        st = gpu_io.GpuStep(dw.online, dw.online.cu[:-1], L, w.A, w.scale)
+        if n_req == w.n_req:
+            S = S_final.clone()
+        else:
+            S = 0.1 * torch.randn((n_req, L.h_v, L.dv, L.dk), device="cuda")
+        for _ in range(3):
+            st.decode(S)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(steps):
+            st.decode(S)
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / steps
+        nbytes = n_req * (2 * L.h_v * L.dv * L.dk * 4 + 2 * L.h_qk * L.dk * io + 2 * L.h_v * L.dv * io
+                          + n_gates * L.h_v * gb)
+        gbs = nbytes / (us * 1e-6) / 1e9
+        res[f"requests_{n_req}"] = dict(avg_us=round(us, 2), algorithmic_bytes=nbytes, achieved_GBs=round(gbs, 1),
+                                        frac=round(gbs / HBM_PEAK_GBS, 4), bound="hbm")
+        log(f"[bench] decode step, {n_req} requests: {us:.2f} us, {gbs:.0f} GB/s")
+    return res
+
+
 # ---------------------------------------------------------------- CPU oracle baseline
 def cpu_baseline(w, budget_s: float):
     """Time the fp64 CPU oracle on request 0 (all heads) and scale to the step."""
@@ -182,6 +227,7 @@ def main():
                     help="workload index (default 3: Gated DeltaNet, 32K context, 4 requests)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of CPU-oracle work")
+    ap.add_argument("--no-decode", action="store_true", help="skip the decode-step timing")
     ap.add_argument("--copy-probe", action="store_true",
                     help="after timing, run a plain 512 MiB device copy (counter calibration)")
     args = ap.parse_args()
@@ -233,6 +279,8 @@ def main():
     per_op = {name: float(np.mean([ev[k][i][0].elapsed_time(ev[k][i][1]) for k in range(args.steps)]))
               for i, (name, _) in enumerate(ops)}
     log("[bench] timed: " + ", ".join(f"{k} {v * 1e3:.1f} us" for k, v in per_op.items()))
+
+    decode = None if args.no_decode else decode_bench(w, G.S_final, args.steps)
 
     if args.copy_probe:
         src = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
@@ -299,6 +347,7 @@ def main():
         "ex_tokens_per_s": round(T / ((per_op["fold"] + per_op["compose"] + per_op["scan"]) * 1e-3), 1),
         "roofline": roofs[dominant],
         "roofline_by_kernel": roofs,
+        "decode_step": decode,
         "cpu_baseline": None,
     }
     if args.copy_probe:

@@ -44,7 +44,7 @@
 extern "C" {
 #endif
 
-#define LKV_ABI_VERSION 1
+#define LKV_ABI_VERSION 2
 
 typedef enum {
     LKV_OK = 0,
@@ -166,6 +166,30 @@ lkv_status lkv_gdn_chunk_scan(const lkv_layer* layer, const lkv_tokens* online, 
  * S_final; y may be NULL.  layer->family must be LKV_SSD. */
 lkv_status lkv_ssd_chunk_scan(const lkv_layer* layer, const lkv_tokens* online,
                               const float* S_init, void* y, float* S_final, void* stream);
+
+/* Decode step: the step that follows the online prefill, which keeps only the
+ * final state for it (Sec. 2).  One new token per request advances each
+ * request's state by one step of the recurrence (Eq. 1) and gives that
+ * token's output, with the post-update state:
+ *   Gated DeltaNet (Eq. 3): S <- alpha S + beta (v - alpha S k) k^T
+ *                           (= S A_t + beta v k^T),  o = scale * S q
+ *   Mamba-2 (Eq. 2):        S <- exp(dt A_h) S + dt x B^T,  y = S C
+ *   q, k   [n_req,h_qk,dk] io_dtype          (SSD: C, B)
+ *   v      [n_req,h_v,dv]  io_dtype          (SSD: x)
+ *   g, beta GDN: [n_req,h_v] gate_dtype, g = log(alpha)
+ *   dt, A  SSD: dt [n_req,H] f32 (> 0), A [H] f32 (< 0)
+ *   S      [n_req,h_v,dv,dk] f32 device, read and updated in place
+ *   o / y  [n_req,h_v,dv] io_dtype, or NULL (state only)
+ * q, k, v and S must be 16-byte aligned.  layer->chunk is not used.  The call
+ * is memory-bound: it reads and writes every state element once.
+ * Errors: LKV_E_NULL, LKV_E_SHAPE, LKV_E_DTYPE, LKV_E_ALIGN, LKV_E_UNSUPPORTED,
+ * LKV_E_HIP. */
+lkv_status lkv_gdn_decode(const lkv_layer* layer, int32_t n_req, const void* q, const void* k,
+                          const void* v, const void* g, const void* beta, float scale, float* S,
+                          void* o, void* stream);
+lkv_status lkv_ssd_decode(const lkv_layer* layer, int32_t n_req, const void* C, const void* B,
+                          const void* x, const float* dt, const float* A, float* S, void* y,
+                          void* stream);
 
 #ifdef __cplusplus
 }

@@ -4,7 +4,7 @@ Only the test-suite, the smoke check and the benchmark's CPU-baseline leg may
 import this package.  It shares no code with the GPU library.
 """
 from .core import (gdn_scan, gdn_transition, ssd_scan, ssd_log_decay, init_single,
-                   compose_gdn, compose_ssd, load)
+                   compose_gdn, compose_ssd, gdn_decode, ssd_decode, load)
 
 __all__ = ["gdn_scan", "gdn_transition", "ssd_scan", "ssd_log_decay", "init_single",
-           "compose_gdn", "compose_ssd", "load"]
+           "compose_gdn", "compose_ssd", "gdn_decode", "ssd_decode", "load"]

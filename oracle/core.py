@@ -157,3 +157,20 @@ def compose_ssd(blk_cu, blk_ids, B_pool, Lam_pool) -> np.ndarray:
     load().lkvo_compose_ssd(n_req, _p(blk_cu), _p(blk_ids), H, P, N, _p(B_pool),
                             _p(Lam_pool), _p(out))
     return out
+
+
+def gdn_decode(q, k, v, g, beta, S, scale: float = 1.0) -> Tuple[np.ndarray, np.ndarray]:
+    """One decode step per request (one token each, Eq. 1 and Eq. 3): the token
+    recurrence run over single-token segments from the requests' states S
+    [n_req,h_v,dv,dk].  Returns (o [n_req,h_v,dv], S_new)."""
+    n_req = np.asarray(k).shape[0]
+    cu = np.arange(n_req + 1, dtype=np.int32)
+    return gdn_scan(cu, q, k, v, g, beta, scale=scale, S0=S)
+
+
+def ssd_decode(C, B, x, dt, A, S) -> Tuple[np.ndarray, np.ndarray]:
+    """One Mamba-2 decode step per request (Eq. 1 and Eq. 2), from states S
+    [n_req,H,P,N].  Returns (y [n_req,H,P], S_new)."""
+    n_req = np.asarray(B).shape[0]
+    cu = np.arange(n_req + 1, dtype=np.int32)
+    return ssd_scan(cu, C, B, x, dt, A, S0=S)

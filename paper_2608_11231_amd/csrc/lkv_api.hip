@@ -2,6 +2,7 @@
 // launch-geometry selection and dispatch to the gfx950 kernels.
 #include <stdlib.h>
 
+#include "decode_kernels.h"
 #include "init_kernels.h"
 #include "lkv.h"
 #include "chunk_kernel.h"
@@ -128,6 +129,32 @@ lkv_status chunk_scan(const lkv_layer* L, const lkv_tokens* T, float scale, cons
     a.nb = nw;
     a.n_units = (int32_t)units;
     return hip_status(launch_scan(L, a, (hipStream_t)stream));
+}
+
+lkv_status decode(const lkv_layer* L, int32_t n_req, const void* q, const void* k, const void* v,
+                  const void* g, const void* beta, const float* A, float scale, float* S, void* o, void* stream) {
+    if (n_req < 0) return LKV_E_SHAPE;
+    if (n_req == 0) return LKV_OK;
+    if (!q || !k || !v || !g || !S || (L->family == LKV_GDN && !beta)) return LKV_E_NULL;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(S)) return LKV_E_ALIGN;
+    if ((int64_t)n_req * L->h_v * (L->dv / 16) >= (INT64_C(1) << 31)) return LKV_E_SHAPE;
+    DecodeArgs a = {};
+    a.n_req = n_req;
+    a.h_qk = L->h_qk;
+    a.h_v = L->h_v;
+    a.dv = L->dv;
+    a.io_bf16 = L->io_dtype == LKV_BF16;
+    a.gate_bf16 = L->gate_dtype == LKV_BF16;
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.g = g;
+    a.beta = beta;
+    a.A = A;
+    a.scale = scale;
+    a.S = S;
+    a.out = o;
+    return hip_status(launch_decode(L->family == LKV_GDN ? 0 : 1, L->dk, a, (hipStream_t)stream));
 }
 
 }  // namespace
@@ -261,6 +288,23 @@ lkv_status lkv_ssd_chunk_scan(const lkv_layer* L, const lkv_tokens* T, const flo
     if (s != LKV_OK) return s;
     if (L->family != LKV_SSD) return LKV_E_SHAPE;
     return chunk_scan(L, T, 1.f, S_init, y, S_final, stream);
+}
+
+lkv_status lkv_gdn_decode(const lkv_layer* L, int32_t n_req, const void* q, const void* k, const void* v,
+                          const void* g, const void* beta, float scale, float* S, void* o, void* stream) {
+    lkv_status s = check_layer(L);
+    if (s != LKV_OK) return s;
+    if (L->family != LKV_GDN) return LKV_E_SHAPE;
+    return decode(L, n_req, q, k, v, g, beta, nullptr, scale, S, o, stream);
+}
+
+lkv_status lkv_ssd_decode(const lkv_layer* L, int32_t n_req, const void* C, const void* B, const void* x,
+                          const float* dt, const float* A, float* S, void* y, void* stream) {
+    lkv_status s = check_layer(L);
+    if (s != LKV_OK) return s;
+    if (L->family != LKV_SSD) return LKV_E_SHAPE;
+    if (n_req > 0 && !A) return LKV_E_NULL;
+    return decode(L, n_req, C, B, x, dt, nullptr, A, 1.f, S, y, stream);
 }
 
 }  // extern "C"

@@ -88,3 +88,32 @@ class GpuWorkload:
                                stream)
         else:
             lkv.ssd_chunk_scan(self.layer, self.online.struct, S_init, self.out, self.S_final, stream)
+
+
+class GpuStep:
+    """One token per request for a decode step: rows ``idx`` of a token stream,
+    gathered on the host and copied to HBM."""
+
+    def __init__(self, tok: I.Tokens, idx: np.ndarray, layer: I.Layer, A: Optional[np.ndarray],
+                 scale: float = 1.0, device="cuda"):
+        io = _TORCH[layer.io_dtype]
+        gate = _TORCH[layer.gate_dtype] if layer.family == I.GDN else torch.float32
+        self.family = layer.family
+        self.layer = layer_struct(layer)
+        self.n_req = int(len(idx))
+        self.scale = scale
+        self.q = _t(tok.q[idx], io, device)
+        self.k = _t(tok.k[idx], io, device)
+        self.v = _t(tok.v[idx], io, device)
+        self.g = _t(tok.g[idx], gate, device)
+        self.beta = _t(tok.beta[idx], gate, device) if tok.beta is not None else None
+        self.A = _t(A, torch.float32, device) if layer.family == I.SSD else None
+        self.out = torch.empty((self.n_req, layer.h_v, layer.dv), device=device, dtype=io)
+
+    def decode(self, S: torch.Tensor, with_out: bool = True, stream=None):
+        """Advance ``S`` [n_req,h_v,dv,dk] by this step in place; the outputs land in ``out``."""
+        o = self.out if with_out else None
+        if self.family == I.GDN:
+            lkv.gdn_decode(self.layer, self.q, self.k, self.v, self.g, self.beta, self.scale, S, o, stream)
+        else:
+            lkv.ssd_decode(self.layer, self.q, self.k, self.v, self.g, self.A, S, o, stream)

@@ -48,7 +48,8 @@ class Tokens(ctypes.Structure):
 _lib = None
 _lock = threading.Lock()
 EXPORTS = ("lkv_abi_version", "lkv_status_string", "lkv_last_hip_error", "lkv_block_summary",
-           "lkv_init_single", "lkv_init_compose", "lkv_gdn_chunk_scan", "lkv_ssd_chunk_scan")
+           "lkv_init_single", "lkv_init_compose", "lkv_gdn_chunk_scan", "lkv_ssd_chunk_scan",
+           "lkv_gdn_decode", "lkv_ssd_decode")
 
 
 def load() -> ctypes.CDLL:
@@ -71,8 +72,10 @@ def load() -> ctypes.CDLL:
             lib.lkv_init_compose.argtypes = [LP, i32, i32, vp, vp, vp, vp, i32, vp, vp]
             lib.lkv_gdn_chunk_scan.argtypes = [LP, TP, f32, vp, vp, vp, vp]
             lib.lkv_ssd_chunk_scan.argtypes = [LP, TP, vp, vp, vp, vp]
+            lib.lkv_gdn_decode.argtypes = [LP, i32, vp, vp, vp, vp, vp, f32, vp, vp, vp]
+            lib.lkv_ssd_decode.argtypes = [LP, i32, vp, vp, vp, vp, vp, vp, vp, vp]
             for f in ("lkv_block_summary", "lkv_init_single", "lkv_init_compose", "lkv_gdn_chunk_scan",
-                      "lkv_ssd_chunk_scan"):
+                      "lkv_ssd_chunk_scan", "lkv_gdn_decode", "lkv_ssd_decode"):
                 getattr(lib, f).restype = ctypes.c_int
             _lib = lib
     return _lib
@@ -153,3 +156,17 @@ def ssd_chunk_scan(layer: Layer, online: Tokens, S_init: Optional[torch.Tensor],
                    S_final: Optional[torch.Tensor], stream=None) -> None:
     _check(load().lkv_ssd_chunk_scan(ctypes.byref(layer), ctypes.byref(online), _ptr(S_init), _ptr(y),
                                      _ptr(S_final), _stream(stream)), "lkv_ssd_chunk_scan")
+
+
+def gdn_decode(layer: Layer, q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, g: torch.Tensor,
+               beta: torch.Tensor, scale: float, S: torch.Tensor, o: Optional[torch.Tensor], stream=None) -> None:
+    """One decode step for every request (``q.shape[0]`` requests); ``S`` is updated in place."""
+    _check(load().lkv_gdn_decode(ctypes.byref(layer), int(q.shape[0]), _ptr(q), _ptr(k), _ptr(v), _ptr(g),
+                                 _ptr(beta), float(scale), _ptr(S), _ptr(o), _stream(stream)), "lkv_gdn_decode")
+
+
+def ssd_decode(layer: Layer, C: torch.Tensor, B: torch.Tensor, x: torch.Tensor, dt: torch.Tensor,
+               A: torch.Tensor, S: torch.Tensor, y: Optional[torch.Tensor], stream=None) -> None:
+    """One Mamba-2 decode step for every request; ``S`` is updated in place."""
+    _check(load().lkv_ssd_decode(ctypes.byref(layer), int(C.shape[0]), _ptr(C), _ptr(B), _ptr(x), _ptr(dt),
+                                 _ptr(A), _ptr(S), _ptr(y), _stream(stream)), "lkv_ssd_decode")

@@ -407,3 +407,67 @@ def test_pins_detect_planted_mistakes():
 
     for kind in ("no_alpha_in_read", "sign", "transposed_write"):
         assert _rel(variant(kind), Sb) > 1e-3
+
+
+# ---------------------------------------------------------------- decode step
+def test_decode_step_matches_dense_transition():
+    """One decode step per request (Eq. 1 with Eq. 3) against an explicit dense
+    transition S A_t + beta v k^T, with grouped heads and distinct requests."""
+    n_req, h_qk, h_v, dk, dv = 3, 2, 4, 6, 5
+    q = _unit(RNG.standard_normal((n_req, h_qk, dk)))
+    k = _unit(RNG.standard_normal((n_req, h_qk, dk)))
+    v = RNG.standard_normal((n_req, h_v, dv))
+    g = np.log(RNG.uniform(0.5, 1.0, (n_req, h_v)))
+    beta = RNG.uniform(0.0, 1.0, (n_req, h_v))
+    S0 = RNG.standard_normal((n_req, h_v, dv, dk))
+    o, S = oracle.gdn_decode(q, k, v, g, beta, S0, scale=0.6)
+    for r in range(n_req):
+        for h in range(h_v):
+            hq = h // (h_v // h_qk)
+            A = np.exp(g[r, h]) * (np.eye(dk) - beta[r, h] * np.outer(k[r, hq], k[r, hq]))
+            Sb = S0[r, h] @ A + beta[r, h] * np.outer(v[r, h], k[r, hq])
+            assert _rel(S[r, h], Sb) < 1e-13
+            assert _rel(o[r, h], 0.6 * Sb @ q[r, hq]) < 1e-13
+
+
+def test_decode_from_zero_state_is_rank_one_write():
+    """From S = 0 one step writes beta v k^T, so o = scale beta (k.q) v."""
+    dk, dv = 8, 3
+    q = _unit(RNG.standard_normal((1, 1, dk)))
+    k = _unit(RNG.standard_normal((1, 1, dk)))
+    v = RNG.standard_normal((1, 1, dv))
+    o, S = oracle.gdn_decode(q, k, v, np.array([[-0.3]]), np.array([[0.4]]),
+                             np.zeros((1, 1, dv, dk)), scale=2.0)
+    assert _rel(S[0, 0], 0.4 * np.outer(v[0, 0], k[0, 0])) < 1e-14
+    assert _rel(o[0, 0], 2.0 * 0.4 * (k[0, 0] @ q[0, 0]) * v[0, 0]) < 1e-14
+
+
+def test_decode_steps_chain_to_one_scan():
+    """T decode steps from S0 equal the brute-force recurrence over the T tokens."""
+    T, dk, dv = 7, 5, 4
+    q, k, v, g, beta = _gdn_slice(T, dk, dv, RNG)
+    S0 = RNG.standard_normal((dv, dk))
+    ob, Sb = _brute_gdn(q, k, v, g, beta, S0, scale=0.9)
+    S = S0[None, None].copy()
+    for t in range(T):
+        o, S = oracle.gdn_decode(q[t][None, None], k[t][None, None], v[t][None, None],
+                                 g[t].reshape(1, 1), beta[t].reshape(1, 1), S, scale=0.9)
+        assert _rel(o[0, 0], ob[t]) < 1e-13
+    assert _rel(S[0, 0], Sb) < 1e-13
+
+
+def test_ssd_decode_closed_form():
+    """Mamba-2 step (Eq. 2): S <- exp(dt A_h) S + dt x B^T, y = S C, per request and head."""
+    n_req, G, H, N, P = 2, 1, 3, 6, 4
+    C = RNG.standard_normal((n_req, G, N))
+    B = RNG.standard_normal((n_req, G, N))
+    x = RNG.standard_normal((n_req, H, P))
+    dt = RNG.uniform(0.01, 0.5, (n_req, H))
+    A = -RNG.uniform(0.5, 3.0, H)
+    S0 = RNG.standard_normal((n_req, H, P, N))
+    y, S = oracle.ssd_decode(C, B, x, dt, A, S0)
+    for r in range(n_req):
+        for h in range(H):
+            Sb = np.exp(dt[r, h] * A[h]) * S0[r, h] + dt[r, h] * np.outer(x[r, h], B[r, 0])
+            assert _rel(S[r, h], Sb) < 1e-13
+            assert _rel(y[r, h], Sb @ C[r, 0]) < 1e-13
