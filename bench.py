@@ -19,7 +19,8 @@ and ``roofline_by_kernel`` for all four.  ``cpu_baseline`` times the CPU oracle
 on a bounded sample of the same workload and scales it to the whole step.
 ``decode_step`` times, after the step and outside it, the decode call that
 follows the prefill (one token per request) on the workload's final states and
-on a 256-request batch.
+on a 256-request batch; ``gather_selected`` times the gather that forms the
+online stream from the cached context at selected positions.
 """
 import argparse
 import json
@@ -148,6 +149,44 @@ def decode_bench(w, S_final, steps: int, batches=(None, 256)):
     return res
 
 
+# ---------------------------------------------------------------- selected-position gather
+def gather_bench(w, G, steps: int):
+    """Time the gather that forms the recompute's online stream from the context:
+    each request's cached context (its blocks, in order) and as many uniformly
+    selected positions as it has online tokens.  The context's q is not part of
+    the cached stream; its k buffer stands in as the q source (same shape and
+    dtype).  Algorithmic bytes = every gathered row read once and written once."""
+    import torch
+    from paper_2608_11231_amd import gpu_io
+    from paper_2608_11231_amd import inputs as I
+    L = w.layer
+    ctx_cu = I.context_cu(w)
+    rng = np.random.default_rng(2608)
+    per = []
+    for r in range(w.n_req):
+        n_ctx = int(ctx_cu[r + 1] - ctx_cu[r])
+        m = int(w.online.cu[r + 1] - w.online.cu[r])
+        per.append(I.select_uniform(rng, n_ctx, m / n_ctx) if n_ctx else np.zeros(0, np.int32))
+    sel_cu, pos = I.pack_selection(per)
+    sel = gpu_io.GpuSelection(G.cached, ctx_cu, sel_cu, pos, L, ctx_q=G.cached.k)
+    for _ in range(3):
+        sel.gather()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(steps):
+        sel.gather()
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / steps
+    row = sum(x.element_size() * x[0].numel() for x in (sel.q, sel.k, sel.v, sel.g, sel.beta) if x is not None)
+    nbytes = 2 * sel.n_sel * row
+    gbs = nbytes / (us * 1e-6) / 1e9
+    log(f"[bench] gather of {sel.n_sel} selected tokens: {us:.2f} us, {gbs:.0f} GB/s")
+    return dict(selected_tokens=sel.n_sel, avg_us=round(us, 2), algorithmic_bytes=nbytes,
+                achieved_GBs=round(gbs, 1), frac=round(gbs / HBM_PEAK_GBS, 4), bound="hbm")
+
+
 # ---------------------------------------------------------------- CPU oracle baseline
 def cpu_baseline(w, budget_s: float):
     """Time the fp64 CPU oracle on request 0 (all heads) and scale to the step."""
@@ -227,7 +266,8 @@ def main():
                     help="workload index (default 3: Gated DeltaNet, 32K context, 4 requests)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of CPU-oracle work")
-    ap.add_argument("--no-decode", action="store_true", help="skip the decode-step timing")
+    ap.add_argument("--no-decode", action="store_true",
+                    help="skip the timings outside the step (decode step, selected-position gather)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="after timing, run a plain 512 MiB device copy (counter calibration)")
     args = ap.parse_args()
@@ -281,6 +321,7 @@ def main():
     log("[bench] timed: " + ", ".join(f"{k} {v * 1e3:.1f} us" for k, v in per_op.items()))
 
     decode = None if args.no_decode else decode_bench(w, G.S_final, args.steps)
+    gather = None if args.no_decode else gather_bench(w, G, args.steps)
 
     if args.copy_probe:
         src = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
@@ -348,6 +389,7 @@ def main():
         "roofline": roofs[dominant],
         "roofline_by_kernel": roofs,
         "decode_step": decode,
+        "gather_selected": gather,
         "cpu_baseline": None,
     }
     if args.copy_probe:

@@ -44,7 +44,7 @@
 extern "C" {
 #endif
 
-#define LKV_ABI_VERSION 2
+#define LKV_ABI_VERSION 3
 
 typedef enum {
     LKV_OK = 0,
@@ -190,6 +190,31 @@ lkv_status lkv_gdn_decode(const lkv_layer* layer, int32_t n_req, const void* q, 
 lkv_status lkv_ssd_decode(const lkv_layer* layer, int32_t n_req, const void* C, const void* B,
                           const void* x, const float* dt, const float* A, float* S, void* y,
                           void* stream);
+
+/* Selected-position gather (Alg. 1, selection and recompute steps): the
+ * recompute runs the recurrence over the selected positions U = {i_1 < ... <
+ * i_m} of each request's context only, in context order (Sec. 3.1), so its
+ * token stream is the context's rows at U.  For request r and every selected
+ * row j in [sel_cu[r], sel_cu[r+1]):
+ *   out row j  =  context row ctx->cu[r] + pos[j]   (bit-exact, each array)
+ *   ctx      the requests' full context streams (n_seq = n_req)
+ *   pos      device int32 [n_sel], positions inside the request's context.
+ *            Context order is the caller's: the call copies in the given
+ *            order and does not sort or check it.  A position outside
+ *            [0, context length) gives NaN rows.
+ *   sel_cu   device int32 [n_req+1] (clamped to [0, n_sel]); rows outside
+ *            every segment get NaN rows
+ *   n_sel    host copy of sel_cu[n_req]
+ *   q, k, v, g, beta  outputs [n_sel, ...] in ctx's dtypes and row shapes;
+ *            each may be NULL (not gathered), and then ctx's may be NULL too.
+ *            SSD: q = C, k = B, v = x, g = dt, beta unused.
+ * The outputs with ctx->A form the online stream of the chunk scan, with
+ * cu = sel_cu.  Outputs must not overlap ctx.  HBM-bound: every gathered byte
+ * is read once and written once.  Errors: LKV_E_NULL, LKV_E_SHAPE,
+ * LKV_E_DTYPE, LKV_E_ALIGN, LKV_E_UNSUPPORTED, LKV_E_HIP. */
+lkv_status lkv_gather_selected(const lkv_layer* layer, const lkv_tokens* ctx, const int32_t* pos,
+                               const int32_t* sel_cu, int64_t n_sel, void* q, void* k, void* v,
+                               void* g, void* beta, void* stream);
 
 #ifdef __cplusplus
 }

@@ -3,6 +3,7 @@
 #include <stdlib.h>
 
 #include "decode_kernels.h"
+#include "gather_kernels.h"
 #include "init_kernels.h"
 #include "lkv.h"
 #include "chunk_kernel.h"
@@ -305,6 +306,48 @@ lkv_status lkv_ssd_decode(const lkv_layer* L, int32_t n_req, const void* C, cons
     if (L->family != LKV_SSD) return LKV_E_SHAPE;
     if (n_req > 0 && !A) return LKV_E_NULL;
     return decode(L, n_req, C, B, x, dt, nullptr, A, 1.f, S, y, stream);
+}
+
+lkv_status lkv_gather_selected(const lkv_layer* L, const lkv_tokens* ctx, const int32_t* pos,
+                               const int32_t* sel_cu, int64_t n_sel, void* q, void* k, void* v, void* g,
+                               void* beta, void* stream) {
+    lkv_status s = check_layer(L);
+    if (s != LKV_OK) return s;
+    if (!ctx) return LKV_E_NULL;
+    if (n_sel < 0 || ctx->n_seq < 0 || ctx->n_tok < 0) return LKV_E_SHAPE;
+    if (n_sel == 0) return LKV_OK;
+    if (n_sel >= (INT64_C(1) << 31)) return LKV_E_SHAPE;
+    if (!pos || !sel_cu || !ctx->cu) return LKV_E_NULL;
+    const int io = L->io_dtype == LKV_BF16 ? 2 : 4;
+    const int gate = (L->family == LKV_GDN && L->gate_dtype == LKV_BF16) ? 2 : 4;
+    GatherArgs a = {};
+    a.ctx_cu = ctx->cu;
+    a.ctx_tok = ctx->n_tok;
+    a.pos = pos;
+    a.sel_cu = sel_cu;
+    a.n_sel = n_sel;
+    a.n_req = ctx->n_seq;
+    const void* src[GATHER_ARRAYS] = {ctx->q, ctx->k, ctx->v, ctx->g, ctx->beta};
+    void* dst[GATHER_ARRAYS] = {q, k, v, g, L->family == LKV_GDN ? beta : nullptr};
+    const int64_t rb[GATHER_ARRAYS] = {(int64_t)L->h_qk * L->dk * io, (int64_t)L->h_qk * L->dk * io,
+                                       (int64_t)L->h_v * L->dv * io, (int64_t)L->h_v * gate,
+                                       (int64_t)L->h_v * gate};
+    const int eb[GATHER_ARRAYS] = {io, io, io, gate, gate};
+    bool any = false;
+    for (int i = 0; i < GATHER_ARRAYS; ++i) {
+        if (!dst[i]) continue;
+        if (!src[i]) return LKV_E_NULL;
+        if (!aligned16(src[i]) || !aligned16(dst[i])) return LKV_E_ALIGN;
+        if (rb[i] >= (INT64_C(1) << 30)) return LKV_E_SHAPE;
+        a.src[i] = src[i];
+        a.dst[i] = dst[i];
+        a.row_bytes[i] = (int32_t)rb[i];
+        a.elem_bytes[i] = eb[i];
+        any = true;
+    }
+    if (!any) return LKV_OK;
+    if (ctx->n_seq == 0) return LKV_E_SHAPE;
+    return hip_status(launch_gather(a, (hipStream_t)stream));
 }
 
 }  // extern "C"

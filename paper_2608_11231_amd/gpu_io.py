@@ -117,3 +117,30 @@ class GpuStep:
             lkv.gdn_decode(self.layer, self.q, self.k, self.v, self.g, self.beta, self.scale, S, o, stream)
         else:
             lkv.ssd_decode(self.layer, self.q, self.k, self.v, self.g, self.A, S, o, stream)
+
+
+class GpuSelection:
+    """The recompute's online stream, gathered on the GPU from a context stream at
+    the selected positions (``sel_cu``, ``pos``); ``struct`` is that stream for
+    the chunk scan.  ``q`` of the context may be given separately (``ctx_q``)."""
+
+    def __init__(self, ctx: GpuTokens, ctx_cu: np.ndarray, sel_cu: np.ndarray, pos: np.ndarray,
+                 layer: I.Layer, ctx_q: Optional[torch.Tensor] = None, device="cuda"):
+        self.layer = layer_struct(layer)
+        self.ctx_cu = _t(ctx_cu, torch.int32, device)
+        cq = ctx.q if ctx_q is None else ctx_q
+        self.ctx_struct = lkv.make_tokens(self.ctx_cu, ctx.n_tok, cq, ctx.k, ctx.v, ctx.g, ctx.beta, ctx.A)
+        self.sel_cu = _t(sel_cu, torch.int32, device)
+        self.pos = _t(pos, torch.int32, device)
+        self.n_sel = int(sel_cu[-1])
+
+        def like(x):
+            return None if x is None else torch.empty((self.n_sel,) + tuple(x.shape[1:]), device=device,
+                                                      dtype=x.dtype)
+        self.q, self.k, self.v, self.g, self.beta = (like(x) for x in (cq, ctx.k, ctx.v, ctx.g, ctx.beta))
+        self.struct = lkv.make_tokens(self.sel_cu, self.n_sel, self.q, self.k, self.v, self.g, self.beta,
+                                      ctx.A)
+
+    def gather(self, stream=None):
+        lkv.gather_selected(self.layer, self.ctx_struct, self.pos, self.sel_cu, self.n_sel, self.q, self.k,
+                            self.v, self.g, self.beta, stream)

@@ -292,6 +292,56 @@ def lengths_capped(rng: np.random.Generator, k: int, lo: int, hi: int, cap: int)
 
 
 # --------------------------------------------------------------------------
+# synthetic selectors (which context positions the recompute replays)
+# --------------------------------------------------------------------------
+
+def select_uniform(rng: np.random.Generator, n_ctx: int, r: float) -> np.ndarray:
+    """A recompute budget r: round(r * n_ctx) distinct positions drawn uniformly,
+    ascending (context order)."""
+    m = int(round(r * n_ctx))
+    return np.sort(rng.choice(n_ctx, size=m, replace=False)).astype(np.int32)
+
+
+def select_seams(block_lens: Sequence[int], window: int) -> np.ndarray:
+    """Seam selection: a window of ``window`` positions around every boundary between
+    consecutive cached blocks (window // 2 before it, the rest after), merged and
+    ascending."""
+    ends = np.cumsum(np.asarray(block_lens, np.int64))
+    n_ctx = int(ends[-1]) if len(ends) else 0
+    keep = np.zeros(n_ctx, bool)
+    for b in ends[:-1]:
+        keep[max(0, b - window // 2):min(n_ctx, b + window - window // 2)] = True
+    return np.nonzero(keep)[0].astype(np.int32)
+
+
+def pack_selection(per_request: Sequence[np.ndarray]):
+    """(sel_cu, pos) of per-request position lists."""
+    cu = np.zeros(len(per_request) + 1, np.int32)
+    cu[1:] = np.cumsum([len(p) for p in per_request])
+    pos = (np.concatenate([np.asarray(p, np.int32) for p in per_request])
+           if per_request else np.zeros(0, np.int32))
+    return cu, pos.astype(np.int32)
+
+
+def context_cu(w: "Workload") -> np.ndarray:
+    """Offsets of each request's context in the cached stream (its blocks are
+    consecutive segments there, in context order)."""
+    assert np.array_equal(w.blk_ids, np.arange(w.n_blk, dtype=np.int32))
+    return w.cached.cu[w.blk_cu].astype(np.int32)
+
+
+def random_block_src(rng: np.random.Generator, w: "Workload") -> np.ndarray:
+    """One uniformly drawn matched block per request (the random-block
+    single-source variant), as pool rows; -1 for a request with no blocks."""
+    src = np.full(w.n_req, -1, np.int32)
+    for r in range(w.n_req):
+        k0, k1 = int(w.blk_cu[r]), int(w.blk_cu[r + 1])
+        if k1 > k0:
+            src[r] = w.blk_ids[int(rng.integers(k0, k1))]
+    return src
+
+
+# --------------------------------------------------------------------------
 # the five reference workloads
 # --------------------------------------------------------------------------
 

@@ -49,7 +49,7 @@ _lib = None
 _lock = threading.Lock()
 EXPORTS = ("lkv_abi_version", "lkv_status_string", "lkv_last_hip_error", "lkv_block_summary",
            "lkv_init_single", "lkv_init_compose", "lkv_gdn_chunk_scan", "lkv_ssd_chunk_scan",
-           "lkv_gdn_decode", "lkv_ssd_decode")
+           "lkv_gdn_decode", "lkv_ssd_decode", "lkv_gather_selected")
 
 
 def load() -> ctypes.CDLL:
@@ -74,8 +74,9 @@ def load() -> ctypes.CDLL:
             lib.lkv_ssd_chunk_scan.argtypes = [LP, TP, vp, vp, vp, vp]
             lib.lkv_gdn_decode.argtypes = [LP, i32, vp, vp, vp, vp, vp, f32, vp, vp, vp]
             lib.lkv_ssd_decode.argtypes = [LP, i32, vp, vp, vp, vp, vp, vp, vp, vp]
+            lib.lkv_gather_selected.argtypes = [LP, TP, vp, vp, ctypes.c_int64, vp, vp, vp, vp, vp, vp]
             for f in ("lkv_block_summary", "lkv_init_single", "lkv_init_compose", "lkv_gdn_chunk_scan",
-                      "lkv_ssd_chunk_scan", "lkv_gdn_decode", "lkv_ssd_decode"):
+                      "lkv_ssd_chunk_scan", "lkv_gdn_decode", "lkv_ssd_decode", "lkv_gather_selected"):
                 getattr(lib, f).restype = ctypes.c_int
             _lib = lib
     return _lib
@@ -170,3 +171,12 @@ def ssd_decode(layer: Layer, C: torch.Tensor, B: torch.Tensor, x: torch.Tensor, 
     """One Mamba-2 decode step for every request; ``S`` is updated in place."""
     _check(load().lkv_ssd_decode(ctypes.byref(layer), int(C.shape[0]), _ptr(C), _ptr(B), _ptr(x), _ptr(dt),
                                  _ptr(A), _ptr(S), _ptr(y), _stream(stream)), "lkv_ssd_decode")
+
+
+def gather_selected(layer: Layer, ctx: Tokens, pos: torch.Tensor, sel_cu: torch.Tensor, n_sel: int,
+                    q: Optional[torch.Tensor], k: Optional[torch.Tensor], v: Optional[torch.Tensor],
+                    g: Optional[torch.Tensor], beta: Optional[torch.Tensor], stream=None) -> None:
+    """Copy the context rows at the selected positions into q/k/v/g/beta (any may be None)."""
+    _check(load().lkv_gather_selected(ctypes.byref(layer), ctypes.byref(ctx), _ptr(pos), _ptr(sel_cu),
+                                      int(n_sel), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta),
+                                      _stream(stream)), "lkv_gather_selected")

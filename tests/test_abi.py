@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_strings(lib):
-    assert lib.lkv_abi_version() == 2
+    assert lib.lkv_abi_version() == 3
     assert lib.lkv_status_string(0) == b"ok"
     assert b"NULL" in lib.lkv_status_string(1)
 
@@ -86,3 +86,33 @@ def test_argument_validation(lib):
     assert lib.lkv_init_single(by(_layer()), 2, 1, None, None, None, None) == 1
     assert lib.lkv_init_compose(by(_layer()), 1, 1, None, None, None, None, 0, None, None) == 1
     assert lib.lkv_init_compose(by(_layer()), 0, 0, None, None, None, None, 0, None, None) == 0
+
+
+
+def test_decode_and_gather_validation(lib):
+    by = ctypes.byref
+    vp = ctypes.c_void_p
+    # decode: family checked per call, empty batch is a no-op, missing tensors
+    assert lib.lkv_ssd_decode(by(_layer()), 1, *([None] * 7), None) == 2
+    assert lib.lkv_gdn_decode(by(_layer()), 0, *([None] * 5), ctypes.c_float(1.0), None, None, None) == 0
+    assert lib.lkv_gdn_decode(by(_layer()), 1, *([None] * 5), ctypes.c_float(1.0), None, None, None) == 1
+    assert lib.lkv_gdn_decode(by(_layer()), -1, *([None] * 5), ctypes.c_float(1.0), None, None, None) == 2
+    a = vp(0x1000)
+    assert lib.lkv_gdn_decode(by(_layer()), 1, a, a, vp(0x1008), a, a, ctypes.c_float(1.0), a, None,
+                              None) == 4
+    # gather: nothing selected is a no-op; a requested array needs its source
+    C = _tokens(1, 10)
+    C.cu = a
+    assert lib.lkv_gather_selected(by(_layer()), by(C), None, None, ctypes.c_int64(0), a, a, a, a, a,
+                                   None) == 0
+    assert lib.lkv_gather_selected(by(_layer()), by(C), a, a, ctypes.c_int64(-1), None, None, None,
+                                   None, None, None) == 2
+    assert lib.lkv_gather_selected(by(_layer()), by(C), a, a, ctypes.c_int64(4), a, None, None, None,
+                                   None, None) == 1
+    C.q = vp(0x1008)
+    assert lib.lkv_gather_selected(by(_layer()), by(C), a, a, ctypes.c_int64(4), a, None, None, None,
+                                   None, None) == 4
+    assert lib.lkv_gather_selected(by(_layer()), by(C), a, a, ctypes.c_int64(4), None, None, None, None,
+                                   None, None) == 0
+    assert lib.lkv_gather_selected(by(_layer()), None, a, a, ctypes.c_int64(4), None, None, None, None,
+                                   None, None) == 1
