@@ -20,7 +20,9 @@ on a bounded sample of the same workload and scales it to the whole step.
 ``decode_step`` times, after the step and outside it, the decode call that
 follows the prefill (one token per request) on the workload's final states and
 on a 256-request batch; ``gather_selected`` times the gather that forms the
-online stream from the cached context at selected positions.
+online stream from the cached context at selected positions;
+``bf16_pool_staging`` times the cache's bf16 storage path (pool rounding,
+host-to-device staging of a batch's rows, overlap with the scan).
 """
 import argparse
 import json
@@ -187,6 +189,61 @@ def gather_bench(w, G, steps: int):
                 achieved_GBs=round(gbs, 1), frac=round(gbs / HBM_PEAK_GBS, 4), bound="hbm")
 
 
+# ---------------------------------------------------------------- bf16 pool and staging
+def staging_bench(w, G, steps: int):
+    """The cache in its stored form (bf16 block states and, for exact composition,
+    the cached key/gate streams, in pinned host memory) and the batch's
+    host-to-device staging: the single-block rows (one per request) vs the
+    exact-composition rows (every block's state plus its token stream).  Also
+    times the fp32 -> bf16 pool rounding, the bf16-pool initialisations, and
+    single-block staging on a side stream while the scan runs."""
+    import torch
+    from paper_2608_11231_amd import gpu_io, lkv
+    L = w.layer
+    Bq = torch.empty(G.B_pool.shape, dtype=torch.bfloat16, device="cuda")
+
+    def timed(fn, n, stream=None):
+        st = stream or torch.cuda.current_stream()
+        fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(st)
+        for _ in range(n):
+            fn()
+        e1.record(st)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / n
+
+    us_round = timed(lambda: lkv.round_bf16(G.B_pool, Bq), steps)
+    hc = gpu_io.HostCache(w, Bq.float().cpu().numpy())
+    sb = gpu_io.StagedBatch(hc, w.blk_ids, w.blk_cu, w.last_blk)
+    side = torch.cuda.Stream()
+    us_single = timed(lambda: sb.stage_single(side), steps, side)
+    us_exact = timed(lambda: sb.stage_exact(side), max(2, steps // 10), side)
+    S = torch.empty_like(G.S_single)
+    us_init1 = timed(lambda: sb.init_single(S), steps)
+    us_initx = timed(lambda: sb.init_compose(S), max(2, steps // 4))
+    us_scan = timed(lambda: G.scan(G.S_exact), steps)
+    main = torch.cuda.current_stream()
+
+    def both():
+        side.wait_stream(main)
+        sb.stage_single(side)
+        G.scan(G.S_exact)
+        main.wait_stream(side)
+    us_both = timed(both, steps)
+    b1, bx = sb.staged_bytes(False), sb.staged_bytes(True)
+    log(f"[bench] staging: single-block rows {b1 / 2**20:.1f} MiB in {us_single:.1f} us, exact-composition "
+        f"rows {bx / 2**20:.1f} MiB in {us_exact:.1f} us; scan {us_scan:.1f} us alone, {us_both:.1f} us "
+        f"with single-block staging alongside")
+    return dict(pool_round_bf16_us=round(us_round, 2),
+                single_block=dict(bytes=b1, h2d_us=round(us_single, 2), GBs=round(b1 / us_single / 1e3, 1),
+                                  init_from_bf16_us=round(us_init1, 2)),
+                exact=dict(bytes=bx, h2d_us=round(us_exact, 2), GBs=round(bx / us_exact / 1e3, 1),
+                           fold_plus_compose_from_bf16_us=round(us_initx, 2)),
+                overlap=dict(scan_us=round(us_scan, 2), scan_with_single_staging_us=round(us_both, 2)))
+
+
 # ---------------------------------------------------------------- CPU oracle baseline
 def cpu_baseline(w, budget_s: float):
     """Time the fp64 CPU oracle on request 0 (all heads) and scale to the step."""
@@ -267,7 +324,7 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of CPU-oracle work")
     ap.add_argument("--no-decode", action="store_true",
-                    help="skip the timings outside the step (decode step, selected-position gather)")
+                    help="skip the timings outside the step (decode, gather, staging)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="after timing, run a plain 512 MiB device copy (counter calibration)")
     args = ap.parse_args()
@@ -322,6 +379,7 @@ def main():
 
     decode = None if args.no_decode else decode_bench(w, G.S_final, args.steps)
     gather = None if args.no_decode else gather_bench(w, G, args.steps)
+    staging = None if (args.no_decode or w.layer.family != I.GDN) else staging_bench(w, G, args.steps)
 
     if args.copy_probe:
         src = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
@@ -390,6 +448,7 @@ def main():
         "roofline_by_kernel": roofs,
         "decode_step": decode,
         "gather_selected": gather,
+        "bf16_pool_staging": staging,
         "cpu_baseline": None,
     }
     if args.copy_probe:

@@ -44,7 +44,7 @@
 extern "C" {
 #endif
 
-#define LKV_ABI_VERSION 3
+#define LKV_ABI_VERSION 4
 
 typedef enum {
     LKV_OK = 0,
@@ -118,7 +118,8 @@ int lkv_last_hip_error(void);
  *   M_out  GDN: [n_blk,h_v,dk,dk] f32, M = A_1...A_L, row-major M[i][j]
  *          SSD: [n_blk,H] f32, the log-decay Lambda = A_h * sum_t dt_t
  * Either output may be NULL (then it is not computed); not both.
- * blocks->q is not read.  Errors: LKV_E_NULL, LKV_E_SHAPE, LKV_E_DTYPE,
+ * blocks->q is not read; for Gated DeltaNet with B_out NULL neither is
+ * blocks->v (it may be NULL).  Errors: LKV_E_NULL, LKV_E_SHAPE, LKV_E_DTYPE,
  * LKV_E_ALIGN, LKV_E_UNSUPPORTED, LKV_E_HIP. */
 lkv_status lkv_block_summary(const lkv_layer* layer, const lkv_tokens* blocks,
                              float* B_out, float* M_out, void* stream);
@@ -190,6 +191,44 @@ lkv_status lkv_gdn_decode(const lkv_layer* layer, int32_t n_req, const void* q, 
 lkv_status lkv_ssd_decode(const lkv_layer* layer, int32_t n_req, const void* C, const void* B,
                           const void* x, const float* dt, const float* A, float* S, void* y,
                           void* stream);
+
+/* bf16 cached-state pool.  The cache stores each block's end state S_local in
+ * bf16 in host memory and loads it at serving time (Sec. 4, environment).
+ * These variants of the two initialisations read B_pool as bf16
+ * [n_blk,h_v,dv,dk] and widen it exactly to fp32 (bf16 -> fp32 appends zero
+ * mantissa bits); everything else, M_pool included (it comes from the online
+ * fold, in fp32), is as in lkv_init_single / lkv_init_compose.  In particular
+ * lkv_init_single_bf16 is a bit-exact widening copy. */
+lkv_status lkv_init_single_bf16(const lkv_layer* layer, int32_t n_req, int32_t n_blk,
+                                const void* B_pool, const int32_t* src_blk, float* S_init,
+                                void* stream);
+lkv_status lkv_init_compose_bf16(const lkv_layer* layer, int32_t n_req, int32_t n_blk,
+                                 const void* B_pool, const float* M_pool,
+                                 const int32_t* blk_ids, const int32_t* blk_cu, int32_t n_ids,
+                                 float* S_init, void* stream);
+
+/* Round n fp32 values (device) to bf16 (device), round to nearest even; NaN
+ * stays NaN (quiet), infinities and signed zeros are kept, values beyond the
+ * bf16 range round to infinity.  This is the storage step of a computed pool
+ * (e.g. lkv_block_summary's B_out) into the cache's bf16 format.  src and dst
+ * 16-byte aligned, not overlapping.  Errors: LKV_E_NULL, LKV_E_SHAPE,
+ * LKV_E_ALIGN, LKV_E_HIP. */
+lkv_status lkv_round_bf16(const float* src, void* dst, int64_t n, void* stream);
+
+/* Host-to-device staging of cache rows (the serving-time load of the cached
+ * artefacts from host memory, Sec. 4; the transfer the paper leaves as future
+ * work, Sec. 4.3): for i < n_rows, dst row i <- src row rows[i], rows being
+ * row_bytes bytes.  src is HOST memory and should be pinned (hipHostMalloc):
+ * then the copies are asynchronous on `stream` and overlap kernels running
+ * on other streams; from pageable memory they are synchronous.  rows is a
+ * HOST int32 array (>= 0, not bounds-checked against src: the caller owns
+ * src's extent); each run of consecutive rows is one copy.  dst is device
+ * memory of n_rows * row_bytes bytes.  Typical use: a batch's single-block
+ * rows (one per request) or its exact-composition rows (K per request),
+ * staged into a compact device pool indexed by the remapped row numbers.
+ * Errors: LKV_E_NULL, LKV_E_SHAPE, LKV_E_HIP. */
+lkv_status lkv_stage_rows(void* dst, const void* src, const int32_t* rows, int32_t n_rows,
+                          int64_t row_bytes, void* stream);
 
 /* Selected-position gather (Alg. 1, selection and recompute steps): the
  * recompute runs the recurrence over the selected positions U = {i_1 < ... <

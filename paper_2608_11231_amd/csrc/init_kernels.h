@@ -5,7 +5,7 @@
 namespace lkv {
 
 struct ComposeArgs {
-    const float* B_pool;   // [n_blk,h_v,dv,dk]
+    const void* B_pool;    // [n_blk,h_v,dv,dk] f32, or bf16 when bf16_pool
     const float* M_pool;   // [n_blk,h_v,dk,dk]
     const int32_t* blk_ids;
     const int32_t* blk_cu;
@@ -14,13 +14,14 @@ struct ComposeArgs {
     int32_t tiles;         // row tiles of 16*nw rows over dv
     int32_t nw;
     int32_t n_units;
+    bool bf16_pool;
 };
 
-hipError_t launch_init_single(int32_t n_req, int32_t n_blk, int64_t per_req, const float* B_pool,
+hipError_t launch_init_single(int32_t n_req, int32_t n_blk, int64_t per_req, const void* B_pool, bool bf16_pool,
                               const int32_t* src, float* S, hipStream_t st);
-hipError_t launch_compose_ssd(int32_t n_req, int32_t n_blk, int32_t H, int64_t per_head, const float* B_pool,
-                              const float* Lam, const int32_t* ids, const int32_t* blk_cu, int32_t n_ids,
-                              float* S, hipStream_t st);
+hipError_t launch_compose_ssd(int32_t n_req, int32_t n_blk, int32_t H, int64_t per_head, const void* B_pool,
+                              bool bf16_pool, const float* Lam, const int32_t* ids, const int32_t* blk_cu,
+                              int32_t n_ids, float* S, hipStream_t st);
 hipError_t launch_compose_gdn(int dk, const ComposeArgs& a, hipStream_t st);
 size_t compose_gdn_lds_bytes(int dk);
 

@@ -7,11 +7,31 @@
 
 namespace lkv {
 
+// ---------------------------------------------------------------- pool rows
+// Four consecutive pool elements widened to fp32: an fp32 pool is read as is, a
+// bf16 pool (the cache's storage format) is widened exactly (bf16 -> fp32 only
+// appends zero mantissa bits).
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+template <bool BF>
+__device__ __forceinline__ f32x4 pool4(const void* base, int64_t elem) {
+    if constexpr (BF) {
+        const u32x2 u = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(
+            reinterpret_cast<const uint16_t*>(base) + elem));
+        return f32x4{__builtin_bit_cast(float, u.x << 16), __builtin_bit_cast(float, u.x & 0xffff0000u),
+                     __builtin_bit_cast(float, u.y << 16), __builtin_bit_cast(float, u.y & 0xffff0000u)};
+    } else {
+        return __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(reinterpret_cast<const float*>(base) + elem));
+    }
+}
+
 // ---------------------------------------------------------------- single block
-// S_init[r] = B_pool[src[r]]: a bit-exact 16-byte-vector copy, HBM-bound.
-// One thread per float4 of the output; request r = index / per_req.
+// S_init[r] = B_pool[src[r]]: a bit-exact 16-byte-vector copy (or exact widening
+// of a bf16 pool), HBM-bound.  One thread per four output elements; request
+// r = index / per_req.
+template <bool BF>
 __global__ __launch_bounds__(256) void init_single_kernel(int32_t n_req, int32_t n_blk, int64_t per_req4,
-                                                          const f32x4* __restrict__ B_pool,
+                                                          const void* __restrict__ B_pool,
                                                           const int32_t* __restrict__ src,
                                                           f32x4* __restrict__ S) {
     const int64_t total = (int64_t)n_req * per_req4;
@@ -21,7 +41,7 @@ __global__ __launch_bounds__(256) void init_single_kernel(int32_t n_req, int32_t
         const int32_t id = src[r];
         f32x4 v;
         if (id >= 0 && id < n_blk) {
-            v = __builtin_nontemporal_load(B_pool + (int64_t)id * per_req4 + e);
+            v = pool4<BF>(B_pool, 4 * ((int64_t)id * per_req4 + e));
         } else {
             const float f = (id == -1) ? 0.f : __builtin_nanf("");
             v = f32x4{f, f, f, f};
@@ -30,22 +50,27 @@ __global__ __launch_bounds__(256) void init_single_kernel(int32_t n_req, int32_t
     }
 }
 
-hipError_t launch_init_single(int32_t n_req, int32_t n_blk, int64_t per_req, const float* B_pool,
+hipError_t launch_init_single(int32_t n_req, int32_t n_blk, int64_t per_req, const void* B_pool, bool bf16_pool,
                               const int32_t* src, float* S, hipStream_t st) {
     const int64_t per4 = per_req / 4;
     const int64_t total = (int64_t)n_req * per4;
     if (total == 0) return hipSuccess;
     int64_t blocks = (total + 255) / 256;
     if (blocks > 256 * 16) blocks = 256 * 16;
-    hipLaunchKernelGGL(init_single_kernel, dim3((unsigned)blocks), dim3(256), 0, st, n_req, n_blk, per4,
-                       reinterpret_cast<const f32x4*>(B_pool), src, reinterpret_cast<f32x4*>(S));
+    if (bf16_pool)
+        hipLaunchKernelGGL(init_single_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, st, n_req, n_blk,
+                           per4, B_pool, src, reinterpret_cast<f32x4*>(S));
+    else
+        hipLaunchKernelGGL(init_single_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, st, n_req, n_blk,
+                           per4, B_pool, src, reinterpret_cast<f32x4*>(S));
     return hipGetLastError();
 }
 
 // ---------------------------------------------------------------- Mamba-2 composition
 // S <- B_{b_1}; S <- exp(Lambda_{b_j}) S + B_{b_j}.  Elementwise over the state.
+template <bool BF>
 __global__ __launch_bounds__(256) void compose_ssd_kernel(int32_t n_req, int32_t n_blk, int32_t H,
-                                                          int64_t per_head4, const f32x4* __restrict__ B_pool,
+                                                          int64_t per_head4, const void* __restrict__ B_pool,
                                                           const float* __restrict__ Lam,
                                                           const int32_t* __restrict__ ids,
                                                           const int32_t* __restrict__ blk_cu, int32_t n_ids,
@@ -63,7 +88,7 @@ __global__ __launch_bounds__(256) void compose_ssd_kernel(int32_t n_req, int32_t
         for (int32_t j = b0; j < b1; ++j) {
             const int32_t id = ids[j];
             if (id < 0 || id >= n_blk) { bad = true; break; }
-            const f32x4 b = B_pool[((int64_t)id * H + h) * per_head4 + e];
+            const f32x4 b = pool4<BF>(B_pool, 4 * (((int64_t)id * H + h) * per_head4 + e));
             if (j == b0) {
                 acc = b;
             } else {
@@ -79,16 +104,16 @@ __global__ __launch_bounds__(256) void compose_ssd_kernel(int32_t n_req, int32_t
     }
 }
 
-hipError_t launch_compose_ssd(int32_t n_req, int32_t n_blk, int32_t H, int64_t per_head, const float* B_pool,
-                              const float* Lam, const int32_t* ids, const int32_t* blk_cu, int32_t n_ids,
-                              float* S, hipStream_t st) {
+hipError_t launch_compose_ssd(int32_t n_req, int32_t n_blk, int32_t H, int64_t per_head, const void* B_pool,
+                              bool bf16_pool, const float* Lam, const int32_t* ids, const int32_t* blk_cu,
+                              int32_t n_ids, float* S, hipStream_t st) {
     const int64_t total = (int64_t)n_req * H * (per_head / 4);
     if (total == 0) return hipSuccess;
     int64_t blocks = (total + 255) / 256;
     if (blocks > 256 * 16) blocks = 256 * 16;
-    hipLaunchKernelGGL(compose_ssd_kernel, dim3((unsigned)blocks), dim3(256), 0, st, n_req, n_blk, H,
-                       per_head / 4, reinterpret_cast<const f32x4*>(B_pool), Lam, ids, blk_cu, n_ids,
-                       reinterpret_cast<f32x4*>(S));
+    auto kern = bf16_pool ? compose_ssd_kernel<true> : compose_ssd_kernel<false>;
+    hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(256), 0, st, n_req, n_blk, H, per_head / 4, B_pool,
+                       Lam, ids, blk_cu, n_ids, reinterpret_cast<f32x4*>(S));
     return hipGetLastError();
 }
 
@@ -111,7 +136,7 @@ struct ComposeLds {
     static __host__ __device__ constexpr size_t bytes() { return size_t(2) * DK * SM * 2; }
 };
 
-template <int DK, int NW>
+template <int DK, int NW, bool BF>
 __global__ __launch_bounds__(64 * NW) void compose_gdn_kernel(ComposeArgs p) {
     constexpr int NTK = DK / 16, SM = ComposeLds<DK>::SM;
     constexpr int NTH = 64 * NW;
@@ -133,8 +158,8 @@ __global__ __launch_bounds__(64 * NW) void compose_gdn_kernel(ComposeArgs p) {
     b1 = b1 < b0 ? b0 : (b1 > p.n_ids ? p.n_ids : b1);
 
     auto valid = [&](int32_t id) { return id >= 0 && id < p.n_blk; };
-    auto b_rows = [&](int32_t id) {
-        return p.B_pool + (((int64_t)id * p.h_v + h) * p.dv + my_row) * DK + 4 * g;
+    auto b_rows = [&](int32_t id) {  // element offset of this lane's B row segment
+        return (((int64_t)id * p.h_v + h) * p.dv + my_row) * DK + 4 * g;
     };
     f32x4 mreg[PER], breg[NTK];
     auto prefetch = [&](int32_t id) {
@@ -144,10 +169,9 @@ __global__ __launch_bounds__(64 * NW) void compose_gdn_kernel(ComposeArgs p) {
             const int idx = tid + i * NTH;
             if (NV % NTH == 0 || idx < NV) mreg[i] = Mj[idx];  // shared by the head's row tiles (L2)
         }
-        const float* Bj = b_rows(id);
+        const int64_t Bj = b_rows(id);
 #pragma unroll
-        for (int nt = 0; nt < NTK; ++nt)
-            breg[nt] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(Bj + 16 * nt));
+        for (int nt = 0; nt < NTK; ++nt) breg[nt] = pool4<BF>(p.B_pool, Bj + 16 * nt);
     };
 
     f32x4 S[NTK];
@@ -159,9 +183,9 @@ __global__ __launch_bounds__(64 * NW) void compose_gdn_kernel(ComposeArgs p) {
         if (!valid(id0)) {
             bad = true;
         } else {
-            const float* B0 = b_rows(id0);
+            const int64_t B0 = b_rows(id0);
 #pragma unroll
-            for (int nt = 0; nt < NTK; ++nt) S[nt] = *reinterpret_cast<const f32x4*>(B0 + 16 * nt);
+            for (int nt = 0; nt < NTK; ++nt) S[nt] = pool4<BF>(p.B_pool, B0 + 16 * nt);
         }
     }
     int32_t id_next = (!bad && b0 + 1 < b1) ? p.blk_ids[b0 + 1] : 0;
@@ -250,7 +274,7 @@ size_t compose_gdn_lds_bytes(int dk) {
 template <int DK, int NW>
 static hipError_t launch_compose_gdn_nw(const ComposeArgs& a, hipStream_t st) {
     const size_t lds = ComposeLds<DK>::bytes();
-    auto kern = compose_gdn_kernel<DK, NW>;
+    auto kern = a.bf16_pool ? compose_gdn_kernel<DK, NW, true> : compose_gdn_kernel<DK, NW, false>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;

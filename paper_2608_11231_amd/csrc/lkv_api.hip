@@ -4,6 +4,7 @@
 
 #include "decode_kernels.h"
 #include "gather_kernels.h"
+#include "pool_kernels.h"
 #include "init_kernels.h"
 #include "lkv.h"
 #include "chunk_kernel.h"
@@ -66,15 +67,16 @@ int pick_nw(int fam, int dk, int chunk, bool f32io, int64_t pairs, int rows, int
     return fallback;
 }
 
-lkv_status check_tokens(const lkv_layer* L, const lkv_tokens* T, bool need_q) {
+lkv_status check_tokens(const lkv_layer* L, const lkv_tokens* T, bool need_q, bool need_v = true) {
     if (!T) return LKV_E_NULL;
     if (T->n_seq < 0 || T->n_tok < 0) return LKV_E_SHAPE;
     if (T->n_seq > 0 && !T->cu) return LKV_E_NULL;
     if (T->n_tok > 0) {
-        if (!T->k || !T->v || !T->g) return LKV_E_NULL;
+        if (!T->k || (need_v && !T->v) || !T->g) return LKV_E_NULL;
         if (need_q && !T->q) return LKV_E_NULL;
         if (L->family == LKV_GDN && !T->beta) return LKV_E_NULL;
-        if (!aligned16(T->k) || !aligned16(T->v) || (need_q && !aligned16(T->q))) return LKV_E_ALIGN;
+        if (!aligned16(T->k) || (need_v && !aligned16(T->v)) || (need_q && !aligned16(T->q)))
+            return LKV_E_ALIGN;
     }
     if (L->family == LKV_SSD && T->n_seq > 0 && !T->A) return LKV_E_NULL;
     if (T->n_tok > INT64_C(1) << 40) return LKV_E_SHAPE;
@@ -158,6 +160,62 @@ lkv_status decode(const lkv_layer* L, int32_t n_req, const void* q, const void* 
     return hip_status(launch_decode(L->family == LKV_GDN ? 0 : 1, L->dk, a, (hipStream_t)stream));
 }
 
+lkv_status init_single(const lkv_layer* L, int32_t n_req, int32_t n_blk, const void* B_pool, bool bf16_pool,
+                       const int32_t* src_blk, float* S_init, void* stream) {
+    lkv_status s = check_layer(L);
+    if (s != LKV_OK) return s;
+    if (n_req < 0 || n_blk < 0) return LKV_E_SHAPE;
+    if (n_req == 0) return LKV_OK;
+    if (!src_blk || !S_init || (n_blk > 0 && !B_pool)) return LKV_E_NULL;
+    if (!aligned16(S_init) || (B_pool && !aligned16(B_pool))) return LKV_E_ALIGN;
+    const int64_t per_req = (int64_t)L->h_v * L->dv * L->dk;
+    return hip_status(launch_init_single(n_req, n_blk, per_req, B_pool, bf16_pool, src_blk, S_init,
+                                         (hipStream_t)stream));
+}
+
+lkv_status init_compose(const lkv_layer* L, int32_t n_req, int32_t n_blk, const void* B_pool, bool bf16_pool,
+                        const float* M_pool, const int32_t* blk_ids, const int32_t* blk_cu, int32_t n_ids,
+                        float* S_init, void* stream) {
+    lkv_status s = check_layer(L);
+    if (s != LKV_OK) return s;
+    if (n_req < 0 || n_blk < 0 || n_ids < 0) return LKV_E_SHAPE;
+    if (n_req == 0) return LKV_OK;
+    if (!blk_cu || !S_init || (n_ids > 0 && !blk_ids)) return LKV_E_NULL;
+    if (n_blk > 0 && (!B_pool || !M_pool)) return LKV_E_NULL;
+    if (!aligned16(S_init) || (B_pool && !aligned16(B_pool)) || (M_pool && !aligned16(M_pool)))
+        return LKV_E_ALIGN;
+    hipStream_t st = (hipStream_t)stream;
+    if (L->family == LKV_SSD) {
+        const int64_t per_head = (int64_t)L->dv * L->dk;
+        return hip_status(launch_compose_ssd(n_req, n_blk, L->h_v, per_head, B_pool, bf16_pool, M_pool, blk_ids,
+                                             blk_cu, n_ids, S_init, st));
+    }
+    const int64_t pairs = (int64_t)n_req * L->h_v;
+    int nw = env_int("LKV_COMPOSE_NW", 0);
+    if (nw != 1 && nw != 2 && nw != 4) {
+        nw = 4;
+        while (nw > 1 && (L->dv % (16 * nw) || pairs * (L->dv / (16 * nw)) < 240)) nw >>= 1;
+    }
+    if (L->dv % (16 * nw)) nw = 1;
+    ComposeArgs a = {};
+    a.B_pool = B_pool;
+    a.bf16_pool = bf16_pool;
+    a.M_pool = M_pool;
+    a.blk_ids = blk_ids;
+    a.blk_cu = blk_cu;
+    a.n_ids = n_ids;
+    a.n_blk = n_blk;
+    a.h_v = L->h_v;
+    a.dv = L->dv;
+    a.S = S_init;
+    a.nw = nw;
+    a.tiles = L->dv / (16 * nw);
+    const int64_t units = pairs * a.tiles;
+    if (units >= (INT64_C(1) << 31)) return LKV_E_SHAPE;
+    a.n_units = (int32_t)units;
+    return hip_status(launch_compose_gdn(L->dk, a, st));
+}
+
 }  // namespace
 
 extern "C" {
@@ -184,7 +242,9 @@ lkv_status lkv_block_summary(const lkv_layer* L, const lkv_tokens* T, float* B_o
     lkv_status s = check_layer(L);
     if (s != LKV_OK) return s;
     if (!B_out && !M_out) return LKV_E_NULL;
-    s = check_tokens(L, T, false);
+    // Gated DeltaNet transitions read no values: v may be NULL when B_out is
+    // (the Mamba-2 gate-sum path runs a state tile and reads them)
+    s = check_tokens(L, T, false, B_out != nullptr || L->family == LKV_SSD);
     if (s != LKV_OK) return s;
     if ((B_out && !aligned16(B_out)) || (M_out && !aligned16(M_out))) return LKV_E_ALIGN;
     if (T->n_seq == 0) return LKV_OK;
@@ -223,56 +283,42 @@ lkv_status lkv_block_summary(const lkv_layer* L, const lkv_tokens* T, float* B_o
 
 lkv_status lkv_init_single(const lkv_layer* L, int32_t n_req, int32_t n_blk, const float* B_pool,
                            const int32_t* src_blk, float* S_init, void* stream) {
-    lkv_status s = check_layer(L);
-    if (s != LKV_OK) return s;
-    if (n_req < 0 || n_blk < 0) return LKV_E_SHAPE;
-    if (n_req == 0) return LKV_OK;
-    if (!src_blk || !S_init || (n_blk > 0 && !B_pool)) return LKV_E_NULL;
-    if (!aligned16(S_init) || (B_pool && !aligned16(B_pool))) return LKV_E_ALIGN;
-    const int64_t per_req = (int64_t)L->h_v * L->dv * L->dk;
-    return hip_status(launch_init_single(n_req, n_blk, per_req, B_pool, src_blk, S_init, (hipStream_t)stream));
+    return init_single(L, n_req, n_blk, B_pool, false, src_blk, S_init, stream);
+}
+
+lkv_status lkv_init_single_bf16(const lkv_layer* L, int32_t n_req, int32_t n_blk, const void* B_pool,
+                                const int32_t* src_blk, float* S_init, void* stream) {
+    return init_single(L, n_req, n_blk, B_pool, true, src_blk, S_init, stream);
 }
 
 lkv_status lkv_init_compose(const lkv_layer* L, int32_t n_req, int32_t n_blk, const float* B_pool,
                             const float* M_pool, const int32_t* blk_ids, const int32_t* blk_cu, int32_t n_ids,
                             float* S_init, void* stream) {
-    lkv_status s = check_layer(L);
-    if (s != LKV_OK) return s;
-    if (n_req < 0 || n_blk < 0 || n_ids < 0) return LKV_E_SHAPE;
-    if (n_req == 0) return LKV_OK;
-    if (!blk_cu || !S_init || (n_ids > 0 && !blk_ids)) return LKV_E_NULL;
-    if (n_blk > 0 && (!B_pool || !M_pool)) return LKV_E_NULL;
-    if (!aligned16(S_init) || (B_pool && !aligned16(B_pool)) || (M_pool && !aligned16(M_pool)))
-        return LKV_E_ALIGN;
-    hipStream_t st = (hipStream_t)stream;
-    if (L->family == LKV_SSD) {
-        const int64_t per_head = (int64_t)L->dv * L->dk;
-        return hip_status(launch_compose_ssd(n_req, n_blk, L->h_v, per_head, B_pool, M_pool, blk_ids, blk_cu,
-                                             n_ids, S_init, st));
-    }
-    const int64_t pairs = (int64_t)n_req * L->h_v;
-    int nw = env_int("LKV_COMPOSE_NW", 0);
-    if (nw != 1 && nw != 2 && nw != 4) {
-        nw = 4;
-        while (nw > 1 && (L->dv % (16 * nw) || pairs * (L->dv / (16 * nw)) < 240)) nw >>= 1;
-    }
-    if (L->dv % (16 * nw)) nw = 1;
-    ComposeArgs a = {};
-    a.B_pool = B_pool;
-    a.M_pool = M_pool;
-    a.blk_ids = blk_ids;
-    a.blk_cu = blk_cu;
-    a.n_ids = n_ids;
-    a.n_blk = n_blk;
-    a.h_v = L->h_v;
-    a.dv = L->dv;
-    a.S = S_init;
-    a.nw = nw;
-    a.tiles = L->dv / (16 * nw);
-    const int64_t units = pairs * a.tiles;
-    if (units >= (INT64_C(1) << 31)) return LKV_E_SHAPE;
-    a.n_units = (int32_t)units;
-    return hip_status(launch_compose_gdn(L->dk, a, st));
+    return init_compose(L, n_req, n_blk, B_pool, false, M_pool, blk_ids, blk_cu, n_ids, S_init, stream);
+}
+
+lkv_status lkv_init_compose_bf16(const lkv_layer* L, int32_t n_req, int32_t n_blk, const void* B_pool,
+                                 const float* M_pool, const int32_t* blk_ids, const int32_t* blk_cu, int32_t n_ids,
+                                 float* S_init, void* stream) {
+    return init_compose(L, n_req, n_blk, B_pool, true, M_pool, blk_ids, blk_cu, n_ids, S_init, stream);
+}
+
+lkv_status lkv_round_bf16(const float* src, void* dst, int64_t n, void* stream) {
+    if (n < 0) return LKV_E_SHAPE;
+    if (n == 0) return LKV_OK;
+    if (!src || !dst) return LKV_E_NULL;
+    if (!aligned16(src) || !aligned16(dst)) return LKV_E_ALIGN;
+    return hip_status(launch_round_bf16(src, dst, n, (hipStream_t)stream));
+}
+
+lkv_status lkv_stage_rows(void* dst, const void* src, const int32_t* rows, int32_t n_rows, int64_t row_bytes,
+                          void* stream) {
+    if (n_rows < 0 || row_bytes < 0) return LKV_E_SHAPE;
+    if (n_rows == 0 || row_bytes == 0) return LKV_OK;
+    if (!dst || !src || !rows) return LKV_E_NULL;
+    for (int32_t i = 0; i < n_rows; ++i)
+        if (rows[i] < 0) return LKV_E_SHAPE;
+    return hip_status(stage_rows(dst, src, rows, n_rows, row_bytes, (hipStream_t)stream));
 }
 
 lkv_status lkv_gdn_chunk_scan(const lkv_layer* L, const lkv_tokens* T, float scale, const float* S_init,

@@ -144,3 +144,105 @@ class GpuSelection:
     def gather(self, stream=None):
         lkv.gather_selected(self.layer, self.ctx_struct, self.pos, self.sel_cu, self.n_sel, self.q, self.k,
                             self.v, self.g, self.beta, stream)
+
+
+def compact_rows(blk_ids: np.ndarray):
+    """The distinct pool rows a batch reads (ascending) and its block ids remapped
+    onto them: ``rows[remapped[i]] == blk_ids[i]``."""
+    rows, remapped = np.unique(np.asarray(blk_ids, np.int64), return_inverse=True)
+    return rows.astype(np.int32), remapped.astype(np.int32)
+
+
+class HostCache:
+    """The cache as the paper keeps it: per-block end states in bf16 and, for exact
+    composition, the cached blocks' key/gate streams (Mamba-2: also x), in
+    pinned host memory."""
+
+    def __init__(self, w: I.Workload, B_bf16: np.ndarray):
+        L = w.layer
+        io = _TORCH[L.io_dtype]
+        gate = _TORCH[L.gate_dtype] if L.family == I.GDN else torch.float32
+
+        def pinned(x, dtype):
+            t = torch.empty(x.shape, dtype=dtype, pin_memory=True)
+            t.copy_(torch.from_numpy(np.ascontiguousarray(x)))
+            return t
+        self.w = w
+        self.B = pinned(B_bf16, torch.bfloat16)          # [n_blk,h_v,dv,dk]
+        c = w.cached
+        self.cu = c.cu.astype(np.int64)
+        self.k = pinned(c.k, io)
+        self.v = pinned(c.v, io) if L.family == I.SSD else None
+        self.g = pinned(c.g, gate)
+        self.beta = pinned(c.beta, gate) if c.beta is not None else None
+
+
+class StagedBatch:
+    """A batch's cache rows moved into HBM by ``lkv_stage_rows`` on ``stream``:
+    the single-block rows (one per request) and, for exact composition, the
+    distinct blocks' states plus their key/gate token streams, compacted."""
+
+    def __init__(self, hc: HostCache, blk_ids: np.ndarray, blk_cu: np.ndarray, last_blk: np.ndarray,
+                 exact: bool = True, device="cuda"):
+        self.hc = hc
+        L = hc.w.layer
+        self.layer = layer_struct(L)
+        self.n_req = len(blk_cu) - 1
+        st = (L.h_v, L.dv, L.dk)
+        self.single_rows = np.asarray(last_blk, np.int32)
+        assert (self.single_rows >= 0).all()
+        self.B_single = torch.empty((self.n_req,) + st, device=device, dtype=torch.bfloat16)
+        self.single_src = torch.arange(self.n_req, dtype=torch.int32, device=device)
+        self.exact = exact
+        if exact:
+            self.rows, remapped = compact_rows(blk_ids)
+            self.blk_ids = torch.from_numpy(remapped).to(device)
+            self.blk_cu = torch.from_numpy(np.asarray(blk_cu, np.int32)).to(device)
+            self.n_ids = int(len(remapped))
+            self.B_exact = torch.empty((len(self.rows),) + st, device=device, dtype=torch.bfloat16)
+            lens = hc.cu[self.rows + 1] - hc.cu[self.rows]
+            self.tok_rows = (np.concatenate([np.arange(hc.cu[b], hc.cu[b + 1]) for b in self.rows])
+                             if len(self.rows) else np.zeros(0)).astype(np.int32)
+            cu = np.zeros(len(self.rows) + 1, np.int32)
+            cu[1:] = np.cumsum(lens)
+            self.cu = torch.from_numpy(cu).to(device)
+            n = int(cu[-1])
+            self.k = torch.empty((n,) + tuple(hc.k.shape[1:]), device=device, dtype=hc.k.dtype)
+            self.g = torch.empty((n,) + tuple(hc.g.shape[1:]), device=device, dtype=hc.g.dtype)
+            self.beta = (torch.empty((n,) + tuple(hc.beta.shape[1:]), device=device, dtype=hc.beta.dtype)
+                         if hc.beta is not None else None)
+            # Mamba-2's gate-sum path reads x as well; Gated DeltaNet's transitions do not
+            self.v = (torch.empty((n,) + tuple(hc.v.shape[1:]), device=device, dtype=hc.v.dtype)
+                      if hc.v is not None else None)
+            self.blocks = lkv.make_tokens(self.cu, n, None, self.k, self.v, self.g, self.beta,
+                                          _t(hc.w.A, torch.float32, device) if L.family == I.SSD else None)
+            f32 = dict(device=device, dtype=torch.float32)
+            self.M = (torch.empty((len(self.rows), L.h_v, L.dk, L.dk), **f32) if L.family == I.GDN
+                      else torch.empty((len(self.rows), L.h_v), **f32))
+
+    def stage_single(self, stream=None):
+        lkv.stage_rows(self.B_single, self.hc.B, self.single_rows, stream)
+
+    def stage_exact(self, stream=None):
+        lkv.stage_rows(self.B_exact, self.hc.B, self.rows, stream)
+        lkv.stage_rows(self.k, self.hc.k, self.tok_rows, stream)
+        if self.v is not None:
+            lkv.stage_rows(self.v, self.hc.v, self.tok_rows, stream)
+        lkv.stage_rows(self.g, self.hc.g, self.tok_rows, stream)
+        if self.beta is not None:
+            lkv.stage_rows(self.beta, self.hc.beta, self.tok_rows, stream)
+
+    def staged_bytes(self, exact: bool) -> int:
+        if not exact:
+            return self.B_single.numel() * 2
+        return sum(t.numel() * t.element_size() for t in (self.B_exact, self.k, self.v, self.g, self.beta)
+                   if t is not None)
+
+    def init_single(self, S, stream=None):
+        lkv.init_single_bf16(self.layer, self.n_req, self.B_single, self.single_src, S, stream)
+
+    def init_compose(self, S, stream=None):
+        """Fold the staged blocks' transitions from their key/gate streams, then compose."""
+        lkv.block_summary(self.layer, self.blocks, None, self.M, stream)
+        lkv.init_compose_bf16(self.layer, len(self.rows), self.B_exact, self.M, self.blk_ids, self.blk_cu,
+                              self.n_ids, S, stream)

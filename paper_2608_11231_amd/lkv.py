@@ -49,7 +49,8 @@ _lib = None
 _lock = threading.Lock()
 EXPORTS = ("lkv_abi_version", "lkv_status_string", "lkv_last_hip_error", "lkv_block_summary",
            "lkv_init_single", "lkv_init_compose", "lkv_gdn_chunk_scan", "lkv_ssd_chunk_scan",
-           "lkv_gdn_decode", "lkv_ssd_decode", "lkv_gather_selected")
+           "lkv_gdn_decode", "lkv_ssd_decode", "lkv_gather_selected", "lkv_init_single_bf16",
+           "lkv_init_compose_bf16", "lkv_round_bf16", "lkv_stage_rows")
 
 
 def load() -> ctypes.CDLL:
@@ -75,8 +76,13 @@ def load() -> ctypes.CDLL:
             lib.lkv_gdn_decode.argtypes = [LP, i32, vp, vp, vp, vp, vp, f32, vp, vp, vp]
             lib.lkv_ssd_decode.argtypes = [LP, i32, vp, vp, vp, vp, vp, vp, vp, vp]
             lib.lkv_gather_selected.argtypes = [LP, TP, vp, vp, ctypes.c_int64, vp, vp, vp, vp, vp, vp]
+            lib.lkv_init_single_bf16.argtypes = [LP, i32, i32, vp, vp, vp, vp]
+            lib.lkv_init_compose_bf16.argtypes = [LP, i32, i32, vp, vp, vp, vp, i32, vp, vp]
+            lib.lkv_round_bf16.argtypes = [vp, vp, ctypes.c_int64, vp]
+            lib.lkv_stage_rows.argtypes = [vp, vp, vp, i32, ctypes.c_int64, vp]
             for f in ("lkv_block_summary", "lkv_init_single", "lkv_init_compose", "lkv_gdn_chunk_scan",
-                      "lkv_ssd_chunk_scan", "lkv_gdn_decode", "lkv_ssd_decode", "lkv_gather_selected"):
+                      "lkv_ssd_chunk_scan", "lkv_gdn_decode", "lkv_ssd_decode", "lkv_gather_selected",
+                      "lkv_init_single_bf16", "lkv_init_compose_bf16", "lkv_round_bf16", "lkv_stage_rows"):
                 getattr(lib, f).restype = ctypes.c_int
             _lib = lib
     return _lib
@@ -180,3 +186,41 @@ def gather_selected(layer: Layer, ctx: Tokens, pos: torch.Tensor, sel_cu: torch.
     _check(load().lkv_gather_selected(ctypes.byref(layer), ctypes.byref(ctx), _ptr(pos), _ptr(sel_cu),
                                       int(n_sel), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta),
                                       _stream(stream)), "lkv_gather_selected")
+
+
+def init_single_bf16(layer: Layer, n_blk: int, B_pool: torch.Tensor, src_blk: torch.Tensor, S_init: torch.Tensor,
+                     stream=None) -> None:
+    """Single-block initial state from a bf16 pool (exact widening)."""
+    assert B_pool.dtype == torch.bfloat16
+    _check(load().lkv_init_single_bf16(ctypes.byref(layer), int(src_blk.shape[0]), int(n_blk), _ptr(B_pool),
+                                       _ptr(src_blk), _ptr(S_init), _stream(stream)), "lkv_init_single_bf16")
+
+
+def init_compose_bf16(layer: Layer, n_blk: int, B_pool: torch.Tensor, M_pool: torch.Tensor, blk_ids: torch.Tensor,
+                      blk_cu: torch.Tensor, n_ids: int, S_init: torch.Tensor, stream=None) -> None:
+    """Exact composition from a bf16 B pool and an fp32 M (Lambda) pool."""
+    assert B_pool.dtype == torch.bfloat16
+    _check(load().lkv_init_compose_bf16(ctypes.byref(layer), int(blk_cu.shape[0]) - 1, int(n_blk), _ptr(B_pool),
+                                        _ptr(M_pool), _ptr(blk_ids), _ptr(blk_cu), int(n_ids), _ptr(S_init),
+                                        _stream(stream)), "lkv_init_compose_bf16")
+
+
+def round_bf16(src: torch.Tensor, dst: torch.Tensor, stream=None) -> None:
+    """dst (bf16) <- src (fp32) rounded to nearest even, elementwise."""
+    assert src.dtype == torch.float32 and dst.dtype == torch.bfloat16 and src.numel() == dst.numel()
+    _check(load().lkv_round_bf16(_ptr(src), _ptr(dst), int(src.numel()), _stream(stream)), "lkv_round_bf16")
+
+
+def stage_rows(dst: torch.Tensor, src: torch.Tensor, rows, stream=None) -> None:
+    """dst[i] <- src[rows[i]] for a host (preferably pinned) ``src`` and device ``dst``;
+    ``rows`` is a host int32 array."""
+    import numpy as np
+    r = np.ascontiguousarray(rows, dtype=np.int32)
+    row_bytes = src[0].numel() * src.element_size() if src.shape[0] else 0
+    assert dst.shape[0] >= len(r) and dst[0].numel() * dst.element_size() == row_bytes
+    if len(r) and r.max() >= src.shape[0]:
+        raise ValueError("row index beyond the source pool")
+    if src.device.type != "cpu" or not src.is_contiguous():
+        raise ValueError("stage_rows: the source pool must be a contiguous host tensor")
+    _check(load().lkv_stage_rows(_ptr(dst), ctypes.c_void_p(src.data_ptr()), r.ctypes.data_as(ctypes.c_void_p),
+                                 len(r), int(row_bytes), _stream(stream)), "lkv_stage_rows")

@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_strings(lib):
-    assert lib.lkv_abi_version() == 3
+    assert lib.lkv_abi_version() == 4
     assert lib.lkv_status_string(0) == b"ok"
     assert b"NULL" in lib.lkv_status_string(1)
 
@@ -116,3 +116,21 @@ def test_decode_and_gather_validation(lib):
                                    None, None) == 0
     assert lib.lkv_gather_selected(by(_layer()), None, a, a, ctypes.c_int64(4), None, None, None, None,
                                    None, None) == 1
+
+
+
+def test_pool_calls_validation(lib):
+    by = ctypes.byref
+    vp = ctypes.c_void_p
+    a = vp(0x1000)
+    assert lib.lkv_round_bf16(None, None, ctypes.c_int64(0), None) == 0
+    assert lib.lkv_round_bf16(a, a, ctypes.c_int64(-1), None) == 2
+    assert lib.lkv_round_bf16(None, a, ctypes.c_int64(8), None) == 1
+    assert lib.lkv_round_bf16(a, vp(0x1002), ctypes.c_int64(8), None) == 4
+    assert lib.lkv_stage_rows(None, None, None, 0, ctypes.c_int64(64), None) == 0
+    assert lib.lkv_stage_rows(a, a, None, 2, ctypes.c_int64(64), None) == 1
+    bad = (ctypes.c_int32 * 2)(0, -3)
+    assert lib.lkv_stage_rows(a, a, bad, 2, ctypes.c_int64(64), None) == 2
+    assert lib.lkv_init_single_bf16(by(_layer()), 0, 1, None, None, None, None) == 0
+    assert lib.lkv_init_single_bf16(by(_layer()), 2, 1, None, None, None, None) == 1
+    assert lib.lkv_init_compose_bf16(by(_layer()), 1, 1, None, None, None, None, 0, None, None) == 1
