@@ -22,7 +22,9 @@ follows the prefill (one token per request) on the workload's final states and
 on a 256-request batch; ``gather_selected`` times the gather that forms the
 online stream from the cached context at selected positions;
 ``bf16_pool_staging`` times the cache's bf16 storage path (pool rounding,
-host-to-device staging of a batch's rows, overlap with the scan).
+host-to-device staging of a batch's rows, overlap with the scan);
+``relative_error_probe`` gives both initial states' relative error against the
+full-prefix state and times the diagnostic kernel.
 """
 import argparse
 import json
@@ -227,9 +229,11 @@ def staging_bench(w, G, steps: int):
     main = torch.cuda.current_stream()
 
     def both():
-        side.wait_stream(main)
-        sb.stage_single(side)
+        # the next batch's rows are staged while this batch's scan runs: the scan is
+        # enqueued first, and the copy carries no cross-stream wait (a copy queued
+        # behind an event of another stream holds the host until that event fires)
         G.scan(G.S_exact)
+        sb.stage_single(side)
         main.wait_stream(side)
     us_both = timed(both, steps)
     b1, bx = sb.staged_bytes(False), sb.staged_bytes(True)
@@ -242,6 +246,48 @@ def staging_bench(w, G, steps: int):
                 exact=dict(bytes=bx, h2d_us=round(us_exact, 2), GBs=round(bx / us_exact / 1e3, 1),
                            fold_plus_compose_from_bf16_us=round(us_initx, 2)),
                 overlap=dict(scan_us=round(us_scan, 2), scan_with_single_staging_us=round(us_both, 2)))
+
+
+# ---------------------------------------------------------------- relative-error probe
+def diag_bench(w, G, steps: int):
+    """The per-layer relative error of both initial states against the full-prefix
+    state S* (the scan of each request's whole cached context from zero), as in
+    the paper's construction-time probe, on this layer's synthetic inputs
+    (first-layer-like: a block's tokens do not depend on what precedes it, so
+    exact composition should land on S*); and the diagnostic kernel's time."""
+    import torch
+    from paper_2608_11231_amd import inputs as I
+    from paper_2608_11231_amd import lkv
+    ctx_cu = I.context_cu(w)
+    cu = torch.from_numpy(ctx_cu).cuda()
+    c = G.cached
+    full = lkv.make_tokens(cu, int(ctx_cu[-1]), None, c.k, c.v, c.g, c.beta, c.A)
+    S_star = torch.empty_like(G.S_exact)
+    if w.layer.family == I.GDN:
+        lkv.gdn_chunk_scan(G.layer, full, 1.0, None, None, S_star)
+    else:
+        lkv.ssd_chunk_scan(G.layer, full, None, None, S_star)
+    G.block_summary(B=False, M=True)
+    G.init_single()
+    G.init_compose()
+    h = w.layer.h_v
+    _, _, rx = lkv.state_rel_error(G.S_exact, S_star, group=h)
+    _, _, r1 = lkv.state_rel_error(G.S_single, S_star, group=h)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        lkv.state_rel_error(G.S_single, S_star, group=h)
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / steps
+    nbytes = 2 * G.S_single.numel() * 4
+    log(f"[bench] layer-0 probe: exact {rx.max().item():.2e}, last block {r1.min().item():.3f}.."
+        f"{r1.max().item():.3f}; diagnostic {us:.2f} us")
+    return dict(rel_exact_vs_full_prefix=[float(x) for x in rx.cpu()],
+                rel_last_block_vs_full_prefix=[float(x) for x in r1.cpu()],
+                kernel_us=round(us, 2), algorithmic_bytes=nbytes,
+                achieved_GBs=round(nbytes / us / 1e3, 1))
 
 
 # ---------------------------------------------------------------- CPU oracle baseline
@@ -324,7 +370,7 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of CPU-oracle work")
     ap.add_argument("--no-decode", action="store_true",
-                    help="skip the timings outside the step (decode, gather, staging)")
+                    help="skip the timings outside the step (decode, gather, staging, probe)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="after timing, run a plain 512 MiB device copy (counter calibration)")
     args = ap.parse_args()
@@ -380,6 +426,7 @@ def main():
     decode = None if args.no_decode else decode_bench(w, G.S_final, args.steps)
     gather = None if args.no_decode else gather_bench(w, G, args.steps)
     staging = None if (args.no_decode or w.layer.family != I.GDN) else staging_bench(w, G, args.steps)
+    diag = None if args.no_decode else diag_bench(w, G, args.steps)
 
     if args.copy_probe:
         src = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
@@ -449,6 +496,7 @@ def main():
         "decode_step": decode,
         "gather_selected": gather,
         "bf16_pool_staging": staging,
+        "relative_error_probe": diag,
         "cpu_baseline": None,
     }
     if args.copy_probe:

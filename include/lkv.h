@@ -44,7 +44,7 @@
 extern "C" {
 #endif
 
-#define LKV_ABI_VERSION 4
+#define LKV_ABI_VERSION 5
 
 typedef enum {
     LKV_OK = 0,
@@ -254,6 +254,26 @@ lkv_status lkv_stage_rows(void* dst, const void* src, const int32_t* rows, int32
 lkv_status lkv_gather_selected(const lkv_layer* layer, const lkv_tokens* ctx, const int32_t* pos,
                                const int32_t* sel_cu, int64_t n_sel, void* q, void* k, void* v,
                                void* g, void* beta, void* stream);
+
+/* Relative-error diagnostic (Sec. 3.2, the probe of the constructed initial
+ * state against the true full-prefix state S*, before any recomputation):
+ * for slice s < n_slices (slice_elems consecutive fp32 values of S and S_ref,
+ * e.g. one (request, head) state),
+ *   sq[2s] = ||S_s - R_s||_F^2,   sq[2s+1] = ||R_s||_F^2     (fp64 sums)
+ *   rel[s] = sqrt(sq[2s]) / sqrt(sq[2s+1])
+ * and, when rel_group is not NULL, for g < n_slices / group over the slices
+ * g*group .. g*group+group-1 (e.g. all heads of one request's layer, the
+ * paper's per-layer figure)
+ *   rel_group[g] = sqrt(sum sq[2s]) / sqrt(sum sq[2s+1]).
+ * IEEE division: a zero reference gives inf, or NaN when S is zero too.
+ * Inputs are device fp32, 16-byte aligned, slice_elems a multiple of 4;
+ * outputs are device fp64 (sq [2*n_slices], rel [n_slices], rel_group
+ * [n_slices/group]).  group must divide n_slices.  With the composed error
+ * e = S - S* the squared norms follow the mismatch recursion of Eq. 7 for
+ * perturbed summaries.  Errors: LKV_E_NULL, LKV_E_SHAPE, LKV_E_ALIGN, LKV_E_HIP. */
+lkv_status lkv_state_rel_error(const float* S, const float* S_ref, int32_t n_slices,
+                               int64_t slice_elems, int32_t group, double* sq, double* rel,
+                               double* rel_group, void* stream);
 
 #ifdef __cplusplus
 }

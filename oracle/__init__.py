@@ -7,7 +7,8 @@ from .core import (gdn_scan, gdn_transition, ssd_scan, ssd_log_decay, init_singl
                    compose_gdn, compose_ssd, gdn_decode, ssd_decode, load)
 from .gather import gather_rows, gather_selected
 from .bf16 import round_bf16
+from .diagnostic import mismatch_recursion, rel_error
 
 __all__ = ["gdn_scan", "gdn_transition", "ssd_scan", "ssd_log_decay", "init_single",
            "compose_gdn", "compose_ssd", "gdn_decode", "ssd_decode", "load", "gather_rows", "gather_selected",
-           "round_bf16"]
+           "round_bf16", "rel_error", "mismatch_recursion"]

@@ -3,6 +3,7 @@
 #include <stdlib.h>
 
 #include "decode_kernels.h"
+#include "diag_kernels.h"
 #include "gather_kernels.h"
 #include "pool_kernels.h"
 #include "init_kernels.h"
@@ -394,6 +395,18 @@ lkv_status lkv_gather_selected(const lkv_layer* L, const lkv_tokens* ctx, const 
     if (!any) return LKV_OK;
     if (ctx->n_seq == 0) return LKV_E_SHAPE;
     return hip_status(launch_gather(a, (hipStream_t)stream));
+}
+
+lkv_status lkv_state_rel_error(const float* S, const float* S_ref, int32_t n_slices, int64_t slice_elems,
+                               int32_t group, double* sq, double* rel, double* rel_group, void* stream) {
+    if (n_slices < 0 || slice_elems < 0) return LKV_E_SHAPE;
+    if (n_slices == 0) return LKV_OK;
+    if (!S || !S_ref || !sq || !rel) return LKV_E_NULL;
+    if (slice_elems % 4 != 0) return LKV_E_SHAPE;
+    if (rel_group && (group < 1 || n_slices % group != 0)) return LKV_E_SHAPE;
+    if (!aligned16(S) || !aligned16(S_ref)) return LKV_E_ALIGN;
+    return hip_status(launch_rel_error(S, S_ref, n_slices, slice_elems, group, sq, rel, rel_group,
+                                       (hipStream_t)stream));
 }
 
 }  // extern "C"

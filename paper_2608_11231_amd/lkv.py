@@ -50,7 +50,7 @@ _lock = threading.Lock()
 EXPORTS = ("lkv_abi_version", "lkv_status_string", "lkv_last_hip_error", "lkv_block_summary",
            "lkv_init_single", "lkv_init_compose", "lkv_gdn_chunk_scan", "lkv_ssd_chunk_scan",
            "lkv_gdn_decode", "lkv_ssd_decode", "lkv_gather_selected", "lkv_init_single_bf16",
-           "lkv_init_compose_bf16", "lkv_round_bf16", "lkv_stage_rows")
+           "lkv_init_compose_bf16", "lkv_round_bf16", "lkv_stage_rows", "lkv_state_rel_error")
 
 
 def load() -> ctypes.CDLL:
@@ -80,9 +80,11 @@ def load() -> ctypes.CDLL:
             lib.lkv_init_compose_bf16.argtypes = [LP, i32, i32, vp, vp, vp, vp, i32, vp, vp]
             lib.lkv_round_bf16.argtypes = [vp, vp, ctypes.c_int64, vp]
             lib.lkv_stage_rows.argtypes = [vp, vp, vp, i32, ctypes.c_int64, vp]
+            lib.lkv_state_rel_error.argtypes = [vp, vp, i32, ctypes.c_int64, i32, vp, vp, vp, vp]
             for f in ("lkv_block_summary", "lkv_init_single", "lkv_init_compose", "lkv_gdn_chunk_scan",
                       "lkv_ssd_chunk_scan", "lkv_gdn_decode", "lkv_ssd_decode", "lkv_gather_selected",
-                      "lkv_init_single_bf16", "lkv_init_compose_bf16", "lkv_round_bf16", "lkv_stage_rows"):
+                      "lkv_init_single_bf16", "lkv_init_compose_bf16", "lkv_round_bf16", "lkv_stage_rows",
+                      "lkv_state_rel_error"):
                 getattr(lib, f).restype = ctypes.c_int
             _lib = lib
     return _lib
@@ -224,3 +226,20 @@ def stage_rows(dst: torch.Tensor, src: torch.Tensor, rows, stream=None) -> None:
         raise ValueError("stage_rows: the source pool must be a contiguous host tensor")
     _check(load().lkv_stage_rows(_ptr(dst), ctypes.c_void_p(src.data_ptr()), r.ctypes.data_as(ctypes.c_void_p),
                                  len(r), int(row_bytes), _stream(stream)), "lkv_stage_rows")
+
+
+def state_rel_error(S: torch.Tensor, S_ref: torch.Tensor, slice_dims: int = 2, group: int = 0, stream=None):
+    """Per-slice (the trailing ``slice_dims`` dims) and, with ``group`` > 0, per-group
+    relative Frobenius error of ``S`` against ``S_ref``.  Returns device fp64 tensors
+    (sq [n,2], rel [n], rel_group [n/group] or None)."""
+    assert S.shape == S_ref.shape and S.dtype == torch.float32 == S_ref.dtype
+    elems = 1
+    for d in S.shape[S.dim() - slice_dims:]:
+        elems *= int(d)
+    n = S.numel() // max(elems, 1)
+    sq = torch.empty((n, 2), dtype=torch.float64, device=S.device)
+    rel = torch.empty((n,), dtype=torch.float64, device=S.device)
+    rg = torch.empty((n // group,), dtype=torch.float64, device=S.device) if group > 0 else None
+    _check(load().lkv_state_rel_error(_ptr(S), _ptr(S_ref), int(n), int(elems), int(group), _ptr(sq), _ptr(rel),
+                                      _ptr(rg), _stream(stream)), "lkv_state_rel_error")
+    return sq, rel, rg

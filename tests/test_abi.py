@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_strings(lib):
-    assert lib.lkv_abi_version() == 4
+    assert lib.lkv_abi_version() == 5
     assert lib.lkv_status_string(0) == b"ok"
     assert b"NULL" in lib.lkv_status_string(1)
 
@@ -134,3 +134,16 @@ def test_pool_calls_validation(lib):
     assert lib.lkv_init_single_bf16(by(_layer()), 0, 1, None, None, None, None) == 0
     assert lib.lkv_init_single_bf16(by(_layer()), 2, 1, None, None, None, None) == 1
     assert lib.lkv_init_compose_bf16(by(_layer()), 1, 1, None, None, None, None, 0, None, None) == 1
+
+
+
+def test_rel_error_validation(lib):
+    vp = ctypes.c_void_p
+    a = vp(0x1000)
+    i64 = ctypes.c_int64
+    assert lib.lkv_state_rel_error(None, None, 0, i64(16), 1, None, None, None, None) == 0
+    assert lib.lkv_state_rel_error(a, a, -1, i64(16), 1, a, a, None, None) == 2
+    assert lib.lkv_state_rel_error(a, None, 2, i64(16), 1, a, a, None, None) == 1
+    assert lib.lkv_state_rel_error(a, a, 2, i64(18), 1, a, a, None, None) == 2
+    assert lib.lkv_state_rel_error(a, a, 3, i64(16), 2, a, a, a, None) == 2
+    assert lib.lkv_state_rel_error(a, vp(0x1004), 2, i64(16), 1, a, a, None, None) == 4
