@@ -363,54 +363,55 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                     }
                 }
             }
+            // Outputs (RT == 1 only) are formed transposed, O^T = S Q^T + U^T P^T:
+            // tile mt holds O[16mt + c16][this wave's rows 4g..4g+3], so each lane
+            // stores 4 consecutive state rows of one token.  S Q^T does not depend
+            // on U: it is formed here, while the B-waves would otherwise wait for
+            // the A-waves at the barrier.
+            f32x4 OT[NTC];
+            if (with_out) {
+                const bf16* Qb = sQ(b);
+#pragma unroll
+                for (int mt = 0; mt < NTC; ++mt) OT[mt] = zero4();
+                if constexpr (NTK == 1) {
+#pragma unroll
+                    for (int mt = 0; mt < NTC; ++mt) {
+                        const bf16* qr = Qb + (16 * mt + c16) * SK + 4 * g;
+                        OT[mt] = mma16(Sh[0][0], lds4(qr), OT[mt]);
+                        if (F32IO) {
+                            OT[mt] = mma16(Sl[0][0], lds4(qr), OT[mt]);
+                            OT[mt] = mma16(Sh[0][0], lds4(qr + KPL), OT[mt]);
+                        }
+                    }
+                } else {
+                    constexpr int NKP = NTK / 2;
+                    bf16x8 qh[NKP][NTC], ql[F32IO ? NKP : 1][NTC];
+#pragma unroll
+                    for (int kp = 0; kp < NKP; ++kp)
+#pragma unroll
+                        for (int mt = 0; mt < NTC; ++mt) {
+                            const bf16* qr = Qb + (16 * mt + c16) * SK + 32 * kp + 8 * g;
+                            qh[kp][mt] = lds8(qr);
+                            if constexpr (F32IO) ql[kp][mt] = lds8(qr + KPL);
+                        }
+                    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                    for (int kp = 0; kp < NKP; ++kp)
+#pragma unroll
+                        for (int mt = 0; mt < NTC; ++mt) {
+                            OT[mt] = mma32(Sh[0][2 * kp], Sh[0][2 * kp + 1], qh[kp][mt], OT[mt]);
+                            if constexpr (F32IO) {
+                                OT[mt] = mma32(Sl[0][2 * kp], Sl[0][2 * kp + 1], qh[kp][mt], OT[mt]);
+                                OT[mt] = mma32(Sh[0][2 * kp], Sh[0][2 * kp + 1], ql[kp][mt], OT[mt]);
+                            }
+                        }
+                }
+            }
             __syncthreads();
             // ================= phase II: substitution, outputs, state update
             {
                 const bf16* Kb = sK(b);
                 const float* G = sG(b);
-                // Outputs (RT == 1 only) are formed transposed, O^T = S Q^T + U^T P^T:
-                // tile mt holds O[16mt + c16][this wave's rows 4g..4g+3], so each lane
-                // stores 4 consecutive state rows of one token.  S Q^T does not depend
-                // on U and is issued first, alongside the substitution chain.
-                f32x4 OT[NTC];
-                if (with_out) {
-                    const bf16* Qb = sQ(b);
-#pragma unroll
-                    for (int mt = 0; mt < NTC; ++mt) OT[mt] = zero4();
-                    if constexpr (NTK == 1) {
-#pragma unroll
-                        for (int mt = 0; mt < NTC; ++mt) {
-                            const bf16* qr = Qb + (16 * mt + c16) * SK + 4 * g;
-                            OT[mt] = mma16(Sh[0][0], lds4(qr), OT[mt]);
-                            if (F32IO) {
-                                OT[mt] = mma16(Sl[0][0], lds4(qr), OT[mt]);
-                                OT[mt] = mma16(Sh[0][0], lds4(qr + KPL), OT[mt]);
-                            }
-                        }
-                    } else {
-                        constexpr int NKP = NTK / 2;
-                        bf16x8 qh[NKP][NTC], ql[F32IO ? NKP : 1][NTC];
-#pragma unroll
-                        for (int kp = 0; kp < NKP; ++kp)
-#pragma unroll
-                            for (int mt = 0; mt < NTC; ++mt) {
-                                const bf16* qr = Qb + (16 * mt + c16) * SK + 32 * kp + 8 * g;
-                                qh[kp][mt] = lds8(qr);
-                                if constexpr (F32IO) ql[kp][mt] = lds8(qr + KPL);
-                            }
-                        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-                        for (int kp = 0; kp < NKP; ++kp)
-#pragma unroll
-                            for (int mt = 0; mt < NTC; ++mt) {
-                                OT[mt] = mma32(Sh[0][2 * kp], Sh[0][2 * kp + 1], qh[kp][mt], OT[mt]);
-                                if constexpr (F32IO) {
-                                    OT[mt] = mma32(Sl[0][2 * kp], Sl[0][2 * kp + 1], qh[kp][mt], OT[mt]);
-                                    OT[mt] = mma32(Sh[0][2 * kp], Sh[0][2 * kp + 1], ql[kp][mt], OT[mt]);
-                                }
-                            }
-                    }
-                }
                 f32x4 U[RT][NTC];
                 bf16x4 Uh[RT][NTC], Ul[RT][NTC];
                 // output blocks P (transposed fragments), independent of U: requested early
