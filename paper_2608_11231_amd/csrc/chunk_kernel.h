@@ -32,7 +32,9 @@
 //   * B-waves (NB, 16 state rows each): chunk c's state chain -- K S^T, the
 //     two-level block substitution for U (32-token halves), the outputs, the
 //     state update -- with the fp32 state held in MFMA accumulator registers.
-// LDS holds two pipeline buffers; two workgroup barriers per chunk.
+// LDS holds two pipeline buffers; two workgroup barriers per chunk.  In the
+// block summary the barriers order LDS traffic only (prefetched loads stay in
+// flight across them); the scan keeps full barriers, which measured faster.
 //
 // Precision: bf16 inputs enter the matrix cores exactly.  fp32 operands of the
 // products that feed the state are split into bf16 hi + lo parts and
@@ -145,6 +147,10 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
     // scalar branches instead of exec-masked divergent regions
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int lane = tid & 63, g = lane >> 4, c16 = lane & 15;
+    auto chunk_barrier = []() {
+        if constexpr (SUMMARY) lds_barrier();
+        else __syncthreads();
+    };
     const bool is_b = w < NB;
     const int wa = w - NB;            // A-wave index
     const int tid_a = tid - 64 * NB;  // thread index among the A-waves
@@ -306,12 +312,12 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                 }
         };
         split_state();
-        __syncthreads();  // prologue: chunk 0 staged by the A-waves
+        chunk_barrier();  // prologue: chunk 0 staged by the A-waves
         for (int ci = 0; ci < nch; ++ci) {
             const int b = ci & 1;
             const int64_t c0 = t0 + (int64_t)ci * CH;
             const int n = (int)((t1 - c0) < CH ? (t1 - c0) : CH);
-            __syncthreads();
+            chunk_barrier();
             // ================= phase I: K S^T and the delta-rule right-hand side
             f32x4 X[RT][NTC];
             {
@@ -407,7 +413,7 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                         }
                 }
             }
-            __syncthreads();
+            chunk_barrier();
             // ================= phase II: substitution, outputs, state update
             {
                 const bf16* Kb = sK(b);
@@ -818,27 +824,27 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                 prefetch(0);
                 commit(0);
             }
-            __syncthreads();
+            chunk_barrier();
             if (nch > 0) {
                 a_work(0);
                 if (nch > 1) prefetch(1);
             }
             for (int ci = 0; ci < nch; ++ci) {
-                __syncthreads();
+                chunk_barrier();
                 if (ci + 1 < nch) commit(ci + 1);
                 if (ci + 2 < nch) prefetch(ci + 2);  // a whole chunk of lead time
-                __syncthreads();
+                chunk_barrier();
                 if (ci + 1 < nch) a_work(ci + 1);
             }
         } else {
-            __syncthreads();
+            chunk_barrier();
             if (nch > 0) a_work(0);
             for (int ci = 0; ci < nch; ++ci) {
-                __syncthreads();
+                chunk_barrier();
                 // chunk ci's inverses, needed by the B-waves after the next barrier
                 diag_solve_all(ci & 1);
                 t_blocks(ci & 1);
-                __syncthreads();
+                chunk_barrier();
                 if (ci + 1 < nch) a_work(ci + 1);
             }
         }
