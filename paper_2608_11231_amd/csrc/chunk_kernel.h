@@ -25,10 +25,11 @@
 //   * A-waves (NA = 4): stage chunk c+1 from registers into LDS and prefetch
 //     chunk c+2 from HBM; then compute chunk c+1's state-independent blocks,
 //     stored pre-split (bf16 hi/lo) and transposed for direct fragment reads:
-//     the masked 16x16 diagonal blocks of I + L and the strictly-lower L blocks.
-//     For Gated DeltaNet one A-wave does not stage: while the B-waves start
-//     chunk c it inverts chunk c's diagonal blocks and combines them into the
-//     off-diagonal blocks of the two 32x32 diagonal blocks of (I + L)^{-1};
+//     the strictly-lower L blocks and the inverses of the 16x16 diagonal blocks
+//     of I + L.  For Gated DeltaNet one A-wave does not stage: it masks and
+//     inverts chunk c+1's diagonal blocks, and while the B-waves start chunk c
+//     it combines chunk c's inverses into the off-diagonal blocks of the two
+//     32x32 diagonal blocks of (I + L)^{-1};
 //   * B-waves (NB, 16 state rows each): chunk c's state chain -- K S^T, the
 //     two-level block substitution for U (32-token halves), the outputs, the
 //     state update -- with the fp32 state held in MFMA accumulator registers.
@@ -607,8 +608,8 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
         }
     } else {
         // ---- A-waves: HBM -> register prefetch and register -> LDS commit of a chunk
-        // Gated DeltaNet: A-waves 0..NA-2 stage tiles; A-wave NA-1 (the solver)
-        // finishes the triangular blocks of the chunk the B-waves are working on.
+        // Gated DeltaNet: A-waves 0..NA-2 stage tiles and build the L blocks; A-wave
+        // NA-1 (the solver) builds the triangular inverses.
         constexpr int NSTG = (FAM == FAM_GDN) ? NA - 1 : NA;
         const bool stager = wa < NSTG;
         KQTile<CH, DK, F32IO, 64 * NSTG> pk, pq;
@@ -617,29 +618,39 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
         float lam_sum = 0.f;
         constexpr int ES = F32IO ? 4 : 2;
         const uint32_t qk_rb = (uint32_t)(p.h_qk * DK * ES), v_rb = (uint32_t)(p.h_v * p.dv * ES);
+        // Chunk loads go through buffer resources that end at the chunk's last
+        // valid row: rows past the segment's end (and lanes past the tile) read
+        // as zero by the hardware range check, so the loads need no branches
+        // and the per-lane offsets are the same for every chunk.
+        const uint32_t gbytes = (FAM == FAM_GDN && p.gate_bf16) ? 2u : 4u;
         auto prefetch = [&](int ci) {
             const int64_t c0 = t0 + (int64_t)ci * CH;
-            const int n = (int)((t1 - c0) < CH ? (t1 - c0) : CH);
+            const uint32_t n = (uint32_t)((t1 - c0) < CH ? (t1 - c0) : CH);
             const int64_t qk_off = (c0 * p.h_qk + hq) * (int64_t)DK * ES;
-            pk.load(reinterpret_cast<const char*>(p.k) + qk_off, qk_rb, n, tid_a);
-            if (with_out) pq.load(reinterpret_cast<const char*>(p.q) + qk_off, qk_rb, n, tid_a);
+            pk.load_buf(make_rsrc(reinterpret_cast<const char*>(p.k) + qk_off, n * qk_rb), 0u, qk_rb, tid_a);
+            if (with_out)
+                pq.load_buf(make_rsrc(reinterpret_cast<const char*>(p.q) + qk_off, n * qk_rb), 0u, qk_rb, tid_a);
             if (load_v)
-                pv.load(reinterpret_cast<const char*>(p.v) + ((c0 * p.h_v + h) * (int64_t)p.dv + row0) * ES, v_rb, n,
-                        tid_a);
-            if (tid_a < CH) {
-                const int64_t gi = (c0 + tid_a) * p.h_v + h;
-                pg = pb = 0u;
-                if (tid_a < n) {
-                    if (FAM == FAM_GDN && p.gate_bf16) {
-                        pg = reinterpret_cast<const uint16_t*>(p.g)[gi];
-                        pb = reinterpret_cast<const uint16_t*>(p.beta)[gi];
-                    } else if (FAM == FAM_GDN) {
-                        pg = reinterpret_cast<const uint32_t*>(p.g)[gi];
-                        pb = reinterpret_cast<const uint32_t*>(p.beta)[gi];
-                    } else {
-                        pg = reinterpret_cast<const uint32_t*>(p.g)[gi];  // dt
-                    }
+                pv.load_buf(make_rsrc(reinterpret_cast<const char*>(p.v) +
+                                          ((c0 * p.h_v + h) * (int64_t)p.dv + row0) * ES,
+                                      n * v_rb),
+                            0u, v_rb, tid_a);
+            // gates: lane t < CH takes token t of the chunk (raw bits, widened at commit)
+            const int64_t g_off = (c0 * p.h_v + h) * (int64_t)gbytes;
+            const uint32_t g_rb = (uint32_t)p.h_v * gbytes;
+            const uint32_t goff = tid_a < CH ? (uint32_t)tid_a * g_rb : 0xffffffffu;
+            const __amdgpu_buffer_rsrc_t rg = make_rsrc(reinterpret_cast<const char*>(p.g) + g_off, n * g_rb);
+            if (FAM == FAM_GDN) {
+                const __amdgpu_buffer_rsrc_t rb = make_rsrc(reinterpret_cast<const char*>(p.beta) + g_off, n * g_rb);
+                if (p.gate_bf16) {
+                    pg = buf_load2(rg, goff);
+                    pb = buf_load2(rb, goff);
+                } else {
+                    pg = buf_load4(rg, goff);
+                    pb = buf_load4(rb, goff);
                 }
+            } else {
+                pg = buf_load4(rg, goff);  // dt
             }
         };
         auto commit = [&](int ci) {
@@ -655,11 +666,10 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
             }
         };
 
-        // Gated DeltaNet: (I + L_mm)^{-1} of the diagonal blocks.  diag_prep (A-wave
-        // mm, while the chunk's other blocks are built) puts the masked diagonal
-        // block mm in LDS; in the next phase the solver wave inverts all of them
-        // by right-looking forward substitution with each block in registers, so
-        // the 16 dependent steps wait on FMAs only.
+        // Gated DeltaNet: (I + L_mm)^{-1} of the diagonal blocks.  The solver wave
+        // puts every masked diagonal block in LDS (diag_prep), then inverts all of
+        // them at once by right-looking forward substitution with each block in
+        // registers, so the 16 dependent steps wait on FMAs only.
         auto diag_prep = [&](int b, const float* gcw, int mt) {
             if constexpr (FAM == FAM_GDN) {
                 const bf16* kr = sK(b) + (16 * mt + c16) * SK;
@@ -802,21 +812,29 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
             }
             wave_lds_sync();
             if constexpr (FAM == FAM_GDN) {
-                // A-wave a masks diagonal block a and builds L blocks a, a + 4, ...
-                if (wa < NTC) diag_prep(b, gcw, wa);
-                using NS = integral_constant<int, NA>;
-                switch (wa) {
-                    case 0: items(integral_constant<int, 0>(), NS(), L_KIND(), b, gcw); break;
-                    case 1: items(integral_constant<int, 1>(), NS(), L_KIND(), b, gcw); break;
-                    case 2: items(integral_constant<int, 2>(), NS(), L_KIND(), b, gcw); break;
-                    default: items(integral_constant<int, 3>(), NS(), L_KIND(), b, gcw); break;
+                if (stager) {
+                    // stager a builds the strictly-lower L blocks a, a + NSTG, ...
+                    using NS = integral_constant<int, NSTG>;
+                    switch (wa) {
+                        case 0: items(integral_constant<int, 0>(), NS(), L_KIND(), b, gcw); break;
+                        case 1: items(integral_constant<int, 1 % NSTG>(), NS(), L_KIND(), b, gcw); break;
+                        default: items(integral_constant<int, 2 % NSTG>(), NS(), L_KIND(), b, gcw); break;
+                    }
+                } else {
+                    // the solver masks every diagonal block, then inverts them all
+#pragma unroll
+                    for (int mt = 0; mt < NTC; ++mt) diag_prep(b, gcw, mt);
+                    wave_lds_sync();
+                    diag_solve_all(b);
                 }
             }
         };
 
         // prologue: chunk 0 staged and its blocks built; chunk 1 in flight.  While
-        // the B-waves run chunk c, the A-waves commit chunk c+1 (loaded during
-        // chunk c-1), issue the loads of chunk c+2, and build chunk c+1's blocks.
+        // the B-waves run chunk c, the stagers commit chunk c+1 (loaded during
+        // chunk c-1), issue the loads of chunk c+2, and build chunk c+1's L
+        // blocks; the solver forms chunk c's T blocks, then masks and inverts
+        // chunk c+1's diagonal blocks.
         // The stagers and the solver also run separate loops (same barrier
         // sequence), so the solver's registers do not overlap the prefetch ones.
         if (stager) {
@@ -841,8 +859,8 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
             if (nch > 0) a_work(0);
             for (int ci = 0; ci < nch; ++ci) {
                 chunk_barrier();
-                // chunk ci's inverses, needed by the B-waves after the next barrier
-                diag_solve_all(ci & 1);
+                // chunk ci's T blocks (its diagonal inverses and L blocks were built
+                // before the barrier), needed by the B-waves after the next barrier
                 t_blocks(ci & 1);
                 chunk_barrier();
                 if (ci + 1 < nch) a_work(ci + 1);

@@ -183,6 +183,24 @@ __device__ __forceinline__ void store_tile_tr(bf16* XT, int plane, f32x4 v, int 
 // (two for fp32 inputs, which are split into bf16 hi / lo planes at commit);
 // the unit's two aligned 4-column runs land at their kq_pos places as two
 // 8-byte LDS writes per plane.  Rows t >= n read as zero.
+// Raw buffer resource over [base, base + bytes): 16-byte loads at offsets at or
+// past the end return zeros (the hardware range check), so tile tails need no
+// branches.  Word 3 is the untyped-access configuration of gfx9-family parts.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ uint32_t buf_load4(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+}
+__device__ __forceinline__ uint32_t buf_load2(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
+}
+__device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+    const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+    return uint4{v[0], v[1], v[2], v[3]};
+}
+
 template <int CH, int DK, bool F32IO, int NTH>
 struct KQTile {
     static constexpr int UPR = DK / 8;                // units per row
@@ -204,6 +222,21 @@ struct KQTile {
             }
             a[i] = x;
             if constexpr (F32IO) b[i] = y;
+        }
+    }
+    // The same through a buffer resource whose range ends at the segment's end:
+    // rows past it (and units past the tile) read as zero without a branch.
+    // chunk_off = byte offset of the chunk's first row from the resource base.
+    __device__ __forceinline__ void load_buf(__amdgpu_buffer_rsrc_t r, uint32_t chunk_off, uint32_t row_bytes,
+                                             int tid) {
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int idx = tid + i * NTH;
+            const int t = idx / UPR, u = idx % UPR;
+            const uint32_t off = (NU % NTH != 0 && idx >= NU) ? 0xffffffffu
+                                                                : chunk_off + (uint32_t)t * row_bytes + ES * 8 * u;
+            a[i] = buf_load16(r, off);
+            if constexpr (F32IO) b[i] = buf_load16(r, off == 0xffffffffu ? off : off + 16);
         }
     }
     // units to LDS rows of stride ds elements (lo plane at dst + pofs for fp32 io)
@@ -251,6 +284,16 @@ struct TileRegs {
             uint4 x = uint4{0u, 0u, 0u, 0u};
             if (idx < NV && t < n) x = *reinterpret_cast<const uint4*>(base + (uint32_t)t * row_bytes + 16u * cv);
             r[i] = x;
+        }
+    }
+    // through a buffer resource ending at the segment's end (see KQTile::load_buf)
+    __device__ __forceinline__ void load_buf(__amdgpu_buffer_rsrc_t rs, uint32_t chunk_off, uint32_t row_bytes,
+                                             int tid) {
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int idx = tid + i * NTH;
+            const int t = idx / VPR, cv = idx % VPR;
+            r[i] = buf_load16(rs, idx < NV ? chunk_off + (uint32_t)t * row_bytes + 16u * cv : 0xffffffffu);
         }
     }
     // row-major into dst (row stride ds elements; lo plane at dst + pofs for fp32 io)
