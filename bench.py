@@ -17,7 +17,9 @@ durations come from HIP events on the stream the library launches on, inside
 the timed region; ``roofline`` is given for the kernel that takes the most time
 and ``roofline_by_kernel`` for all four.  ``cpu_baseline`` times the CPU oracle
 on a bounded sample of the same workload and scales it to the whole step.
-``decode_step`` times, after the step and outside it, the decode call that
+``lb_fused_*`` times LinearKV's path as a single launch (the scan reading its
+initial state straight from the cached pool row).  ``decode_step`` times, after
+the step and outside it, the decode call that
 follows the prefill (one token per request) on the workload's final states and
 on a 256-request batch; ``gather_selected`` times the gather that forms the
 online stream from the cached context at selected positions;
@@ -423,6 +425,22 @@ def main():
               for i, (name, _) in enumerate(ops)}
     log("[bench] timed: " + ", ".join(f"{k} {v * 1e3:.1f} us" for k, v in per_op.items()))
 
+    # LinearKV's path as one launch: the scan starting from the cached pool row
+    from paper_2608_11231_amd import lkv
+    fused = lambda: lkv.chunk_scan_from_pool(G.layer, G.online.struct, w.scale, G.B_pool, w.n_blk, G.last_blk,
+                                             G.out, G.S_final)
+    for _ in range(3):
+        fused()
+    f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    f0.record()
+    for _ in range(args.steps):
+        fused()
+    f1.record()
+    torch.cuda.synchronize()
+    fused_us = f0.elapsed_time(f1) * 1e3 / args.steps
+    log(f"[bench] LinearKV path in one launch (scan from the pool row): {fused_us:.1f} us")
+
     decode = None if args.no_decode else decode_bench(w, G.S_final, args.steps)
     gather = None if args.no_decode else gather_bench(w, G, args.steps)
     staging = None if (args.no_decode or w.layer.family != I.GDN) else staging_bench(w, G, args.steps)
@@ -490,6 +508,8 @@ def main():
         "single_init_latency_us": round(per_op["init_single"] * 1e3, 2),
         "scan_us": round(per_op["scan"] * 1e3, 2),
         "lb_tokens_per_s": round(T / ((per_op["init_single"] + per_op["scan"]) * 1e-3), 1),
+        "lb_fused_us": round(fused_us, 2),
+        "lb_fused_tokens_per_s": round(T / (fused_us * 1e-6), 1),
         "ex_tokens_per_s": round(T / ((per_op["fold"] + per_op["compose"] + per_op["scan"]) * 1e-3), 1),
         "roofline": roofs[dominant],
         "roofline_by_kernel": roofs,

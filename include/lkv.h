@@ -44,7 +44,7 @@
 extern "C" {
 #endif
 
-#define LKV_ABI_VERSION 5
+#define LKV_ABI_VERSION 6
 
 typedef enum {
     LKV_OK = 0,
@@ -167,6 +167,23 @@ lkv_status lkv_gdn_chunk_scan(const lkv_layer* layer, const lkv_tokens* online, 
  * S_final; y may be NULL.  layer->family must be LKV_SSD. */
 lkv_status lkv_ssd_chunk_scan(const lkv_layer* layer, const lkv_tokens* online,
                               const float* S_init, void* y, float* S_final, void* stream);
+
+/* LinearKV's path in one launch: the chunk scan of lkv_gdn_chunk_scan /
+ * lkv_ssd_chunk_scan (by layer->family) whose initial state for request r is
+ * the cached state B_pool[src_blk[r]] itself, read by the scan kernel (Sec.
+ * 3.2, single-block initialisation; App. A for other choices of the block).
+ * The results are bit-identical to lkv_init_single (or lkv_init_single_bf16)
+ * followed by the scan from its output, without the intermediate state buffer.
+ *   B_pool     [n_blk,h_v,dv,dk] device, pool_dtype LKV_F32 or LKV_BF16 (widened
+ *              exactly); may be NULL when n_blk = 0
+ *   src_blk    device int32 [online->n_seq]: -1 gives a zero start, any other
+ *              value outside [0, n_blk) a NaN state
+ *   scale      Gated DeltaNet output scale (ignored for Mamba-2)
+ *   out, S_final as for the scans.
+ * Errors: as for the scans, plus LKV_E_DTYPE for an unknown pool_dtype. */
+lkv_status lkv_chunk_scan_from_pool(const lkv_layer* layer, const lkv_tokens* online, float scale,
+                                    const void* B_pool, int32_t pool_dtype, int32_t n_blk,
+                                    const int32_t* src_blk, void* out, float* S_final, void* stream);
 
 /* Decode step: the step that follows the online prefill, which keeps only the
  * final state for it (Sec. 2).  One new token per request advances each

@@ -66,6 +66,9 @@ struct ScanArgs {
     int32_t gate_bf16;   // GDN gates stored as bf16
     float scale;
     const float* S_init;  // scan: [n_seq,h_v,dv,dk] or null
+    const int32_t* src;   // scan: when set, segment s starts from pool row src[s] of S_init
+    int32_t n_src;        //   ([n_src,h_v,dv,dk]; -1 -> zero state, other ids outside -> NaN)
+    int32_t init_bf16;    //   S_init holds bf16 values (widened exactly)
     void* out;            // scan: o / y [n_tok,h_v,dv] or null
     float* S_final;       // scan: final state; summary: B_out (may be null)
     float* M_out;         // summary: GDN M [n_seq,h_v,dk,dk] / SSD Lambda [n_seq,h_v], or null
@@ -287,14 +290,33 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
         // acc layout: S[rt][nt] holds S[row][16nt + 4g + r]
         auto row_of = [&](int rt) { return row0 + 16 * (RT * w + rt) + c16; };
         f32x4 S[RT][NTK];
+        // initial state row: segment s's own (S_init) or, with src, a pool row
+        // (LinearKV's single cached state read straight from the cache pool)
+        int64_t init_row = s;
+        float init_fill = 0.f;
+        bool init_load = !SUMMARY && p.S_init;
+        if (!SUMMARY && p.src) {
+            const int32_t id = p.src[s];
+            init_row = id;
+            if (id < 0 || id >= p.n_src) {
+                init_load = false;
+                init_fill = id == -1 ? 0.f : __builtin_nanf("");
+            }
+        }
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
             for (int nt = 0; nt < NTK; ++nt) {
                 const int row = row_of(rt);
-                if (!SUMMARY && p.S_init) {
-                    S[rt][nt] = *reinterpret_cast<const f32x4*>(
-                        p.S_init + ((int64_t(s) * p.h_v + h) * p.dv + row) * DK + 16 * nt + 4 * g);
+                const int64_t e = ((init_row * p.h_v + h) * p.dv + row) * DK + 16 * nt + 4 * g;
+                if (init_load && p.init_bf16) {
+                    const uint2 u = *reinterpret_cast<const uint2*>(reinterpret_cast<const uint16_t*>(p.S_init) + e);
+                    S[rt][nt] = f32x4{__builtin_bit_cast(float, u.x << 16), __builtin_bit_cast(float, u.x & 0xffff0000u),
+                                      __builtin_bit_cast(float, u.y << 16), __builtin_bit_cast(float, u.y & 0xffff0000u)};
+                } else if (init_load) {
+                    S[rt][nt] = *reinterpret_cast<const f32x4*>(p.S_init + e);
+                } else if (!SUMMARY && p.src) {
+                    S[rt][nt] = f32x4{init_fill, init_fill, init_fill, init_fill};
                 } else {
 #pragma unroll
                     for (int r = 0; r < 4; ++r) S[rt][nt][r] = (mtile && row == 16 * nt + 4 * g + r) ? 1.f : 0.f;

@@ -110,7 +110,8 @@ hipError_t launch_scan(const lkv_layer* L, const ScanArgs& a, hipStream_t st) {
 }
 
 lkv_status chunk_scan(const lkv_layer* L, const lkv_tokens* T, float scale, const float* S_init, void* out,
-                      float* S_final, void* stream) {
+                      float* S_final, void* stream, const int32_t* src = nullptr, int32_t n_src = 0,
+                      bool init_bf16 = false) {
     lkv_status s = check_tokens(L, T, out != nullptr);
     if (s != LKV_OK) return s;
     if ((S_init && !aligned16(S_init)) || (S_final && !aligned16(S_final))) return LKV_E_ALIGN;
@@ -125,6 +126,9 @@ lkv_status chunk_scan(const lkv_layer* L, const lkv_tokens* T, float scale, cons
     ScanArgs a = base_args(L, T);
     a.scale = scale;
     a.S_init = S_init;
+    a.src = src;
+    a.n_src = n_src;
+    a.init_bf16 = init_bf16 ? 1 : 0;
     a.out = out;
     a.S_final = S_final;
     a.summary = 0;
@@ -407,6 +411,22 @@ lkv_status lkv_state_rel_error(const float* S, const float* S_ref, int32_t n_sli
     if (!aligned16(S) || !aligned16(S_ref)) return LKV_E_ALIGN;
     return hip_status(launch_rel_error(S, S_ref, n_slices, slice_elems, group, sq, rel, rel_group,
                                        (hipStream_t)stream));
+}
+
+lkv_status lkv_chunk_scan_from_pool(const lkv_layer* L, const lkv_tokens* T, float scale, const void* B_pool,
+                                    int32_t pool_dtype, int32_t n_blk, const int32_t* src_blk, void* out,
+                                    float* S_final, void* stream) {
+    lkv_status s = check_layer(L);
+    if (s != LKV_OK) return s;
+    if (!T) return LKV_E_NULL;
+    if (n_blk < 0) return LKV_E_SHAPE;
+    if (pool_dtype != LKV_F32 && pool_dtype != LKV_BF16) return LKV_E_DTYPE;
+    if (T->n_seq > 0 && !src_blk) return LKV_E_NULL;
+    if (n_blk > 0 && !B_pool) return LKV_E_NULL;
+    if (B_pool && !aligned16(B_pool)) return LKV_E_ALIGN;
+    // with n_blk = 0 every id is -1 (zero state) or invalid (NaN): the pool is never read
+    return chunk_scan(L, T, L->family == LKV_GDN ? scale : 1.f, reinterpret_cast<const float*>(B_pool), out,
+                      S_final, stream, src_blk, n_blk, pool_dtype == LKV_BF16);
 }
 
 }  // extern "C"

@@ -50,7 +50,8 @@ _lock = threading.Lock()
 EXPORTS = ("lkv_abi_version", "lkv_status_string", "lkv_last_hip_error", "lkv_block_summary",
            "lkv_init_single", "lkv_init_compose", "lkv_gdn_chunk_scan", "lkv_ssd_chunk_scan",
            "lkv_gdn_decode", "lkv_ssd_decode", "lkv_gather_selected", "lkv_init_single_bf16",
-           "lkv_init_compose_bf16", "lkv_round_bf16", "lkv_stage_rows", "lkv_state_rel_error")
+           "lkv_init_compose_bf16", "lkv_round_bf16", "lkv_stage_rows", "lkv_state_rel_error",
+           "lkv_chunk_scan_from_pool")
 
 
 def load() -> ctypes.CDLL:
@@ -81,10 +82,11 @@ def load() -> ctypes.CDLL:
             lib.lkv_round_bf16.argtypes = [vp, vp, ctypes.c_int64, vp]
             lib.lkv_stage_rows.argtypes = [vp, vp, vp, i32, ctypes.c_int64, vp]
             lib.lkv_state_rel_error.argtypes = [vp, vp, i32, ctypes.c_int64, i32, vp, vp, vp, vp]
+            lib.lkv_chunk_scan_from_pool.argtypes = [LP, TP, f32, vp, i32, i32, vp, vp, vp, vp]
             for f in ("lkv_block_summary", "lkv_init_single", "lkv_init_compose", "lkv_gdn_chunk_scan",
                       "lkv_ssd_chunk_scan", "lkv_gdn_decode", "lkv_ssd_decode", "lkv_gather_selected",
                       "lkv_init_single_bf16", "lkv_init_compose_bf16", "lkv_round_bf16", "lkv_stage_rows",
-                      "lkv_state_rel_error"):
+                      "lkv_state_rel_error", "lkv_chunk_scan_from_pool"):
                 getattr(lib, f).restype = ctypes.c_int
             _lib = lib
     return _lib
@@ -243,3 +245,13 @@ def state_rel_error(S: torch.Tensor, S_ref: torch.Tensor, slice_dims: int = 2, g
     _check(load().lkv_state_rel_error(_ptr(S), _ptr(S_ref), int(n), int(elems), int(group), _ptr(sq), _ptr(rel),
                                       _ptr(rg), _stream(stream)), "lkv_state_rel_error")
     return sq, rel, rg
+
+
+def chunk_scan_from_pool(layer: Layer, online: Tokens, scale: float, B_pool: Optional[torch.Tensor], n_blk: int,
+                         src_blk: torch.Tensor, out: Optional[torch.Tensor], S_final: Optional[torch.Tensor],
+                         stream=None) -> None:
+    """The chunk scan starting each request from its cached pool row B_pool[src_blk[r]]."""
+    dt = BF16 if (B_pool is not None and B_pool.dtype == torch.bfloat16) else F32
+    _check(load().lkv_chunk_scan_from_pool(ctypes.byref(layer), ctypes.byref(online), float(scale), _ptr(B_pool), dt,
+                                           int(n_blk), _ptr(src_blk), _ptr(out), _ptr(S_final), _stream(stream)),
+           "lkv_chunk_scan_from_pool")

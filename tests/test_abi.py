@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_strings(lib):
-    assert lib.lkv_abi_version() == 5
+    assert lib.lkv_abi_version() == 6
     assert lib.lkv_status_string(0) == b"ok"
     assert b"NULL" in lib.lkv_status_string(1)
 
@@ -147,3 +147,18 @@ def test_rel_error_validation(lib):
     assert lib.lkv_state_rel_error(a, a, 2, i64(18), 1, a, a, None, None) == 2
     assert lib.lkv_state_rel_error(a, a, 3, i64(16), 2, a, a, a, None) == 2
     assert lib.lkv_state_rel_error(a, vp(0x1004), 2, i64(16), 1, a, a, None, None) == 4
+
+
+
+def test_scan_from_pool_validation(lib):
+    by = ctypes.byref
+    vp = ctypes.c_void_p
+    T = _tokens()
+    f = ctypes.c_float(1.0)
+    assert lib.lkv_chunk_scan_from_pool(by(_layer()), by(T), f, None, 0, 0, None, None, None, None) == 0
+    assert lib.lkv_chunk_scan_from_pool(by(_layer()), by(T), f, None, 7, 0, None, None, None, None) == 3
+    assert lib.lkv_chunk_scan_from_pool(by(_layer()), by(T), f, None, 0, -1, None, None, None, None) == 2
+    assert lib.lkv_chunk_scan_from_pool(by(_layer()), by(T), f, None, 0, 2, None, None, None, None) == 1
+    T1 = _tokens(1, 10)
+    assert lib.lkv_chunk_scan_from_pool(by(_layer()), by(T1), f, None, 0, 0, None, None, None, None) == 1
+    assert lib.lkv_chunk_scan_from_pool(by(_layer()), by(T), f, vp(0x1008), 0, 1, None, None, None, None) == 4

@@ -255,3 +255,43 @@ def test_tiny_config_end_to_end():
         torch.cuda.synchronize()
         assert rel_slices(_np(G.S_final), Sf_ref) < STATE_TOL
         assert rel_slices(_np(G.out)[None], o_ref[None], lead=1) < STATE_TOL
+
+
+@pytest.mark.parametrize("fam,bf", [(I.GDN, False), (I.GDN, True), (I.SSD, False), (I.SSD, True)])
+def test_scan_from_pool_matches_init_then_scan(fam, bf):
+    """LinearKV's one-launch path (the scan reading its start from the pool row) is
+    bit-identical to the single-block initialisation followed by the scan; -1 starts
+    from zero and an invalid id gives NaN."""
+    case = GDN_CASES[1] if fam == I.GDN else SSD_CASES[2]
+    w = _work(fam, case)
+    # four requests: reuse the workload's online stream by repeating its segments
+    G = gpu_io.GpuWorkload(w)
+    G.block_summary(B=True, M=False)
+    pool = G.B_pool.to(torch.bfloat16) if bf else G.B_pool
+    n_req = w.n_req
+    src = np.array([w.n_blk - 1, -1][:n_req] + [0] * max(0, n_req - 2), np.int32)
+    src_d = torch.from_numpy(src).cuda()
+    S_ref = torch.empty_like(G.S_single)
+    if bf:
+        lkv.init_single_bf16(G.layer, w.n_blk, pool, src_d, S_ref)
+    else:
+        lkv.init_single(G.layer, w.n_blk, pool, src_d, S_ref)
+    G.scan(S_ref)
+    torch.cuda.synchronize()
+    out_ref, SF_ref = G.out.clone(), G.S_final.clone()
+    G.out.zero_()
+    G.S_final.zero_()
+    lkv.chunk_scan_from_pool(G.layer, G.online.struct, w.scale, pool, w.n_blk, src_d, G.out, G.S_final)
+    torch.cuda.synchronize()
+    ob = (lambda t: t.view(torch.int16)) if G.out.dtype == torch.bfloat16 else (lambda t: t.view(torch.int32))
+    assert torch.equal(ob(G.out), ob(out_ref))
+    assert torch.equal(G.S_final.view(torch.int32), SF_ref.view(torch.int32))
+    # an invalid id: that request's state and outputs are NaN, the others unchanged
+    src_bad = src.copy()
+    src_bad[0] = w.n_blk + 5
+    lkv.chunk_scan_from_pool(G.layer, G.online.struct, w.scale, pool, w.n_blk, torch.from_numpy(src_bad).cuda(),
+                             G.out, G.S_final)
+    torch.cuda.synchronize()
+    assert torch.isnan(G.S_final[0]).all()
+    if n_req > 1:
+        assert torch.equal(G.S_final[1:].view(torch.int32), SF_ref[1:].view(torch.int32))
