@@ -118,8 +118,8 @@ int lkv_last_hip_error(void);
  *   M_out  GDN: [n_blk,h_v,dk,dk] f32, M = A_1...A_L, row-major M[i][j]
  *          SSD: [n_blk,H] f32, the log-decay Lambda = A_h * sum_t dt_t
  * Either output may be NULL (then it is not computed); not both.
- * blocks->q is not read; for Gated DeltaNet with B_out NULL neither is
- * blocks->v (it may be NULL).  Errors: LKV_E_NULL, LKV_E_SHAPE, LKV_E_DTYPE,
+ * blocks->q is not read; with B_out NULL neither is blocks->v (it may be
+ * NULL), and for Mamba-2 only dt and A are read (k may be NULL too).  Errors: LKV_E_NULL, LKV_E_SHAPE, LKV_E_DTYPE,
  * LKV_E_ALIGN, LKV_E_UNSUPPORTED, LKV_E_HIP. */
 lkv_status lkv_block_summary(const lkv_layer* layer, const lkv_tokens* blocks,
                              float* B_out, float* M_out, void* stream);

@@ -104,6 +104,37 @@ __global__ __launch_bounds__(256) void compose_ssd_kernel(int32_t n_req, int32_t
     }
 }
 
+// ---------------------------------------------------------------- Mamba-2 block transitions
+// Lambda = A_h * sum_t dt_t over each block (the scalar transition of Eq. 5):
+// a segmented sum over the block's dt column, coalesced across heads.  A
+// workgroup covers 64 heads of one block with 4 token lanes per head.
+__global__ __launch_bounds__(256) void ssd_lambda_kernel(const int32_t* __restrict__ cu, int32_t n_seq, int64_t n_tok,
+                                                         int32_t H, const float* __restrict__ dt,
+                                                         const float* __restrict__ A, float* __restrict__ Lam) {
+    __shared__ float part[4][64];
+    const int hg = blockIdx.x % ((H + 63) / 64);
+    const int s = blockIdx.x / ((H + 63) / 64);
+    const int tl = threadIdx.x >> 6, hl = threadIdx.x & 63;
+    const int h = hg * 64 + hl;
+    int64_t t0 = cu[s], t1 = cu[s + 1];
+    t0 = t0 < 0 ? 0 : (t0 > n_tok ? n_tok : t0);
+    t1 = t1 < t0 ? t0 : (t1 > n_tok ? n_tok : t1);
+    float acc = 0.f;
+    if (h < H)
+        for (int64_t t = t0 + tl; t < t1; t += 4) acc += dt[t * H + h];
+    part[tl][hl] = acc;
+    __syncthreads();
+    if (tl == 0 && h < H) Lam[(int64_t)s * H + h] = A[h] * ((part[0][hl] + part[1][hl]) + (part[2][hl] + part[3][hl]));
+}
+
+hipError_t launch_ssd_lambda(const int32_t* cu, int32_t n_seq, int64_t n_tok, int32_t H, const float* dt,
+                             const float* A, float* Lam, hipStream_t st) {
+    const int64_t grid = (int64_t)n_seq * ((H + 63) / 64);
+    if (grid == 0) return hipSuccess;
+    hipLaunchKernelGGL(ssd_lambda_kernel, dim3((unsigned)grid), dim3(256), 0, st, cu, n_seq, n_tok, H, dt, A, Lam);
+    return hipGetLastError();
+}
+
 hipError_t launch_compose_ssd(int32_t n_req, int32_t n_blk, int32_t H, int64_t per_head, const void* B_pool,
                               bool bf16_pool, const float* Lam, const int32_t* ids, const int32_t* blk_cu,
                               int32_t n_ids, float* S, hipStream_t st) {

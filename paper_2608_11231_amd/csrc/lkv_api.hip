@@ -68,15 +68,16 @@ int pick_nw(int fam, int dk, int chunk, bool f32io, int64_t pairs, int rows, int
     return fallback;
 }
 
-lkv_status check_tokens(const lkv_layer* L, const lkv_tokens* T, bool need_q, bool need_v = true) {
+lkv_status check_tokens(const lkv_layer* L, const lkv_tokens* T, bool need_q, bool need_v = true,
+                        bool need_k = true) {
     if (!T) return LKV_E_NULL;
     if (T->n_seq < 0 || T->n_tok < 0) return LKV_E_SHAPE;
     if (T->n_seq > 0 && !T->cu) return LKV_E_NULL;
     if (T->n_tok > 0) {
-        if (!T->k || (need_v && !T->v) || !T->g) return LKV_E_NULL;
+        if ((need_k && !T->k) || (need_v && !T->v) || !T->g) return LKV_E_NULL;
         if (need_q && !T->q) return LKV_E_NULL;
         if (L->family == LKV_GDN && !T->beta) return LKV_E_NULL;
-        if (!aligned16(T->k) || (need_v && !aligned16(T->v)) || (need_q && !aligned16(T->q)))
+        if ((need_k && !aligned16(T->k)) || (need_v && !aligned16(T->v)) || (need_q && !aligned16(T->q)))
             return LKV_E_ALIGN;
     }
     if (L->family == LKV_SSD && T->n_seq > 0 && !T->A) return LKV_E_NULL;
@@ -247,9 +248,9 @@ lkv_status lkv_block_summary(const lkv_layer* L, const lkv_tokens* T, float* B_o
     lkv_status s = check_layer(L);
     if (s != LKV_OK) return s;
     if (!B_out && !M_out) return LKV_E_NULL;
-    // Gated DeltaNet transitions read no values: v may be NULL when B_out is
-    // (the Mamba-2 gate-sum path runs a state tile and reads them)
-    s = check_tokens(L, T, false, B_out != nullptr || L->family == LKV_SSD);
+    // transitions read no values: v may be NULL when B_out is; Mamba-2's
+    // transitions read only dt (and A)
+    s = check_tokens(L, T, false, B_out != nullptr, B_out != nullptr || L->family == LKV_GDN);
     if (s != LKV_OK) return s;
     if ((B_out && !aligned16(B_out)) || (M_out && !aligned16(M_out))) return LKV_E_ALIGN;
     if (T->n_seq == 0) return LKV_OK;
@@ -264,15 +265,10 @@ lkv_status lkv_block_summary(const lkv_layer* L, const lkv_tokens* T, float* B_o
     a.M_out = M_out;
     hipStream_t st = (hipStream_t)stream;
     if (L->family == LKV_SSD && !B_out) {
-        // Lambda only: one row tile per (block, head) carries the gate sum
-        a.nb = 1;
-        a.tiles_b = 1;
-        a.tiles_m = 0;
-        a.S_final = nullptr;
-        const int64_t units = pairs;
-        if (units >= (INT64_C(1) << 31)) return LKV_E_SHAPE;
-        a.n_units = (int32_t)units;
-        return hip_status(launch_scan(L, a, st));
+        // Lambda only: a segmented sum of the dt column, no state work
+        if (pairs >= (INT64_C(1) << 31)) return LKV_E_SHAPE;
+        return hip_status(launch_ssd_lambda(T->cu, T->n_seq, T->n_tok, L->h_v, reinterpret_cast<const float*>(T->g),
+                                            T->A, M_out, st));
     }
     const int nw = pick_nw(L->family, L->dk, L->chunk, f32io, pairs, rows_b ? rows_b : rows_m,
                            rows_b ? rows_m : 0, true);

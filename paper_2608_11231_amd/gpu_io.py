@@ -155,7 +155,7 @@ def compact_rows(blk_ids: np.ndarray):
 
 class HostCache:
     """The cache as the paper keeps it: per-block end states in bf16 and, for exact
-    composition, the cached blocks' key/gate streams (Mamba-2: also x), in
+    composition, the cached blocks' key/gate streams (Mamba-2: dt only), in
     pinned host memory."""
 
     def __init__(self, w: I.Workload, B_bf16: np.ndarray):
@@ -171,8 +171,8 @@ class HostCache:
         self.B = pinned(B_bf16, torch.bfloat16)          # [n_blk,h_v,dv,dk]
         c = w.cached
         self.cu = c.cu.astype(np.int64)
-        self.k = pinned(c.k, io)
-        self.v = pinned(c.v, io) if L.family == I.SSD else None
+        # Gated DeltaNet transitions need the keys and both gates; Mamba-2's only dt
+        self.k = pinned(c.k, io) if L.family == I.GDN else None
         self.g = pinned(c.g, gate)
         self.beta = pinned(c.beta, gate) if c.beta is not None else None
 
@@ -207,14 +207,12 @@ class StagedBatch:
             cu[1:] = np.cumsum(lens)
             self.cu = torch.from_numpy(cu).to(device)
             n = int(cu[-1])
-            self.k = torch.empty((n,) + tuple(hc.k.shape[1:]), device=device, dtype=hc.k.dtype)
+            self.k = (torch.empty((n,) + tuple(hc.k.shape[1:]), device=device, dtype=hc.k.dtype)
+                      if hc.k is not None else None)
             self.g = torch.empty((n,) + tuple(hc.g.shape[1:]), device=device, dtype=hc.g.dtype)
             self.beta = (torch.empty((n,) + tuple(hc.beta.shape[1:]), device=device, dtype=hc.beta.dtype)
                          if hc.beta is not None else None)
-            # Mamba-2's gate-sum path reads x as well; Gated DeltaNet's transitions do not
-            self.v = (torch.empty((n,) + tuple(hc.v.shape[1:]), device=device, dtype=hc.v.dtype)
-                      if hc.v is not None else None)
-            self.blocks = lkv.make_tokens(self.cu, n, None, self.k, self.v, self.g, self.beta,
+            self.blocks = lkv.make_tokens(self.cu, n, None, self.k, None, self.g, self.beta,
                                           _t(hc.w.A, torch.float32, device) if L.family == I.SSD else None)
             f32 = dict(device=device, dtype=torch.float32)
             self.M = (torch.empty((len(self.rows), L.h_v, L.dk, L.dk), **f32) if L.family == I.GDN
@@ -225,9 +223,8 @@ class StagedBatch:
 
     def stage_exact(self, stream=None):
         lkv.stage_rows(self.B_exact, self.hc.B, self.rows, stream)
-        lkv.stage_rows(self.k, self.hc.k, self.tok_rows, stream)
-        if self.v is not None:
-            lkv.stage_rows(self.v, self.hc.v, self.tok_rows, stream)
+        if self.k is not None:
+            lkv.stage_rows(self.k, self.hc.k, self.tok_rows, stream)
         lkv.stage_rows(self.g, self.hc.g, self.tok_rows, stream)
         if self.beta is not None:
             lkv.stage_rows(self.beta, self.hc.beta, self.tok_rows, stream)
@@ -235,7 +232,7 @@ class StagedBatch:
     def staged_bytes(self, exact: bool) -> int:
         if not exact:
             return self.B_single.numel() * 2
-        return sum(t.numel() * t.element_size() for t in (self.B_exact, self.k, self.v, self.g, self.beta)
+        return sum(t.numel() * t.element_size() for t in (self.B_exact, self.k, self.g, self.beta)
                    if t is not None)
 
     def init_single(self, S, stream=None):

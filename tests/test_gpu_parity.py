@@ -295,3 +295,21 @@ def test_scan_from_pool_matches_init_then_scan(fam, bf):
     assert torch.isnan(G.S_final[0]).all()
     if n_req > 1:
         assert torch.equal(G.S_final[1:].view(torch.int32), SF_ref[1:].view(torch.int32))
+
+
+@pytest.mark.parametrize("case", SSD_CASES, ids=[f"ssd{c[:4]}" for c in SSD_CASES])
+def test_ssd_lambda_only(case):
+    """Mamba-2 transitions alone (no B_out): the segmented dt sum, from dt and A only
+    (k and v may be absent), against the oracle and the combined summary."""
+    w = _work(I.SSD, case)
+    G = gpu_io.GpuWorkload(w)
+    c = G.cached
+    blocks = lkv.make_tokens(c.cu, c.n_tok, None, None, None, c.g, None, c.A)
+    lam = torch.empty((w.n_blk, w.layer.h_v), device="cuda")
+    lkv.block_summary(G.layer, blocks, None, lam)
+    G.block_summary(B=True, M=True)
+    torch.cuda.synchronize()
+    _, ref = R.summaries(w)
+    got = _np(lam)
+    assert np.max(np.abs(got - ref) / np.maximum(np.abs(ref), 1e-30)) < STATE_TOL
+    assert np.max(np.abs(got - _np(G.M_pool)) / np.maximum(np.abs(ref), 1e-30)) < STATE_TOL
