@@ -106,12 +106,17 @@ __global__ __launch_bounds__(256) void compose_ssd_kernel(int32_t n_req, int32_t
 
 // ---------------------------------------------------------------- Mamba-2 block transitions
 // Lambda = A_h * sum_t dt_t over each block (the scalar transition of Eq. 5):
-// a segmented sum over the block's dt column, coalesced across heads.  A
-// workgroup covers 64 heads of one block with 4 token lanes per head.
-__global__ __launch_bounds__(256) void ssd_lambda_kernel(const int32_t* __restrict__ cu, int32_t n_seq, int64_t n_tok,
-                                                         int32_t H, const float* __restrict__ dt,
-                                                         const float* __restrict__ A, float* __restrict__ Lam) {
-    __shared__ float part[4][64];
+// a segmented sum over the block's dt rows.  A workgroup covers 64 heads of
+// one block with 16 token lanes (one wave each, so every load is one dt row
+// segment of 256 bytes); each lane keeps several loads in flight, and the 16
+// partial sums are added in a fixed order (reproducible results).
+constexpr int LAM_LANES = 16;
+__global__ __launch_bounds__(64 * LAM_LANES) void ssd_lambda_kernel(const int32_t* __restrict__ cu, int32_t n_seq,
+                                                                    int64_t n_tok, int32_t H,
+                                                                    const float* __restrict__ dt,
+                                                                    const float* __restrict__ A,
+                                                                    float* __restrict__ Lam) {
+    __shared__ float part[LAM_LANES][64];
     const int hg = blockIdx.x % ((H + 63) / 64);
     const int s = blockIdx.x / ((H + 63) / 64);
     const int tl = threadIdx.x >> 6, hl = threadIdx.x & 63;
@@ -119,19 +124,31 @@ __global__ __launch_bounds__(256) void ssd_lambda_kernel(const int32_t* __restri
     int64_t t0 = cu[s], t1 = cu[s + 1];
     t0 = t0 < 0 ? 0 : (t0 > n_tok ? n_tok : t0);
     t1 = t1 < t0 ? t0 : (t1 > n_tok ? n_tok : t1);
-    float acc = 0.f;
-    if (h < H)
-        for (int64_t t = t0 + tl; t < t1; t += 4) acc += dt[t * H + h];
-    part[tl][hl] = acc;
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    if (h < H) {
+        int64_t t = t0 + tl;
+        for (; t + 3 * LAM_LANES < t1; t += 4 * LAM_LANES) {
+#pragma unroll
+            for (int u = 0; u < 4; ++u) acc[u] += dt[(t + u * LAM_LANES) * H + h];
+        }
+        for (; t < t1; t += LAM_LANES) acc[0] += dt[t * H + h];
+    }
+    part[tl][hl] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
     __syncthreads();
-    if (tl == 0 && h < H) Lam[(int64_t)s * H + h] = A[h] * ((part[0][hl] + part[1][hl]) + (part[2][hl] + part[3][hl]));
+    if (tl == 0 && h < H) {
+        float sum = 0.f;
+#pragma unroll
+        for (int i = 0; i < LAM_LANES; ++i) sum += part[i][hl];
+        Lam[(int64_t)s * H + h] = A[h] * sum;
+    }
 }
 
 hipError_t launch_ssd_lambda(const int32_t* cu, int32_t n_seq, int64_t n_tok, int32_t H, const float* dt,
                              const float* A, float* Lam, hipStream_t st) {
     const int64_t grid = (int64_t)n_seq * ((H + 63) / 64);
     if (grid == 0) return hipSuccess;
-    hipLaunchKernelGGL(ssd_lambda_kernel, dim3((unsigned)grid), dim3(256), 0, st, cu, n_seq, n_tok, H, dt, A, Lam);
+    hipLaunchKernelGGL(ssd_lambda_kernel, dim3((unsigned)grid), dim3(64 * LAM_LANES), 0, st, cu, n_seq, n_tok, H, dt,
+                       A, Lam);
     return hipGetLastError();
 }
 

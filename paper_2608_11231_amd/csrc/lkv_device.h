@@ -155,8 +155,6 @@ __device__ __forceinline__ int xcd_unit(int b, int n) {
     return x * q + min(x, r) + i;
 }
 
-// Memory fence + instruction barrier for one wave's own LDS traffic: orders a
-// wave's LDS writes before its later LDS reads of other lanes' data.
 // Workgroup barrier for LDS traffic: waits for this wave's LDS operations only,
 // so global loads issued before it stay in flight across it (a __syncthreads
 // would also drain them).  Only for barriers that order LDS accesses.
@@ -164,6 +162,8 @@ __device__ __forceinline__ void lds_barrier() {
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// Memory fence + instruction barrier for one wave's own LDS traffic: orders a
+// wave's LDS writes before its later LDS reads of other lanes' data.
 __device__ __forceinline__ void wave_lds_sync() {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
