@@ -118,7 +118,9 @@ struct ChunkLds {
     static constexpr size_t GC_OFF = 2 * BUF;      // per A-wave gate prefix
     static constexpr size_t INV_OFF = GC_OFF + al(NA * 64 * 4);
     static constexpr int INV_BST = 16 * SLD + 4;      // f32 stride of inverse scratch blocks (bank shift)
-    static constexpr size_t BYTES = INV_OFF + (HAS_L ? al(size_t(NTC) * INV_BST * 4) : 0);
+    // count of stager signals "this chunk's masked diagonal blocks are in LDS"
+    static constexpr size_t CNT_OFF = INV_OFF + (HAS_L ? al(size_t(NTC) * INV_BST * 4) : 0);
+    static constexpr size_t BYTES = CNT_OFF + (HAS_L ? 16 : 0);
 };
 
 // index of block (mt, nt) among the strictly-lower blocks (nt < mt) / lower blocks (nt <= mt)
@@ -158,6 +160,10 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
     const bool is_b = w < NB;
     const int wa = w - NB;            // A-wave index
     const int tid_a = tid - 64 * NB;  // thread index among the A-waves
+    if constexpr (FAM == FAM_GDN) {
+        // stager -> solver signal count (ordered before its first use by the prologue barrier)
+        if (tid == 0) *reinterpret_cast<uint32_t*>(smem + Ly::CNT_OFF) = 0u;
+    }
 
     // ---- work unit
     const int tiles = p.tiles_b + p.tiles_m;
@@ -657,10 +663,11 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                                           ((c0 * p.h_v + h) * (int64_t)p.dv + row0) * ES,
                                       n * v_rb),
                             0u, v_rb, tid_a);
-            // gates: lane t < CH takes token t of the chunk (raw bits, widened at commit)
+            // gates: lane t < CH of every stager takes token t of the chunk (raw
+            // bits, widened at commit; each stager forms the gate prefix itself)
             const int64_t g_off = (c0 * p.h_v + h) * (int64_t)gbytes;
             const uint32_t g_rb = (uint32_t)p.h_v * gbytes;
-            const uint32_t goff = tid_a < CH ? (uint32_t)tid_a * g_rb : 0xffffffffu;
+            const uint32_t goff = lane < CH ? (uint32_t)lane * g_rb : 0xffffffffu;
             const __amdgpu_buffer_rsrc_t rg = make_rsrc(reinterpret_cast<const char*>(p.g) + g_off, n * g_rb);
             if (FAM == FAM_GDN) {
                 const __amdgpu_buffer_rsrc_t rb = make_rsrc(reinterpret_cast<const char*>(p.beta) + g_off, n * g_rb);
@@ -687,51 +694,108 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                 G[CH + tid_a] = __builtin_bit_cast(float, b16 ? pb << 16 : pb);
             }
         };
-
-        // Gated DeltaNet: (I + L_mm)^{-1} of the diagonal blocks.  The solver wave
-        // puts every masked diagonal block in LDS (diag_prep), then inverts all of
-        // them at once by right-looking forward substitution with each block in
-        // registers, so the 16 dependent steps wait on FMAs only.
-        auto diag_prep = [&](int b, const float* gcw, int mt) {
-            if constexpr (FAM == FAM_GDN) {
-                const bf16* kr = sK(b) + (16 * mt + c16) * SK;
-                const float* G = sG(b);
-                float* INV = reinterpret_cast<float*>(smem + Ly::INV_OFF) + mt * Ly::INV_BST;
-                f32x4 acc = zero4();
-                if constexpr (NK == 1) {
-                    acc = mma16(lds4(kr + 4 * g), lds4(kr + 4 * g), acc);
-                    if (F32IO) {
-                        acc = mma16(lds4(kr + 4 * g), lds4(kr + KPL + 4 * g), acc);
-                        acc = mma16(lds4(kr + KPL + 4 * g), lds4(kr + 4 * g), acc);
-                    }
-                } else {
-                    constexpr int NKP = NK / 2;
-                    bf16x8 kv[NKP], lv[F32IO ? NKP : 1];
-#pragma unroll
-                    for (int kp = 0; kp < NKP; ++kp) {
-                        kv[kp] = lds8(kr + 32 * kp + 8 * g);
-                        if constexpr (F32IO) lv[kp] = lds8(kr + KPL + 32 * kp + 8 * g);
-                    }
-                    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-                    for (int kp = 0; kp < NKP; ++kp) {
-                        acc = mma32(kv[kp], kv[kp], acc);
-                        if constexpr (F32IO) {
-                            acc = mma32(kv[kp], lv[kp], acc);
-                            acc = mma32(lv[kp], kv[kp], acc);
-                        }
-                    }
+        // Per-chunk gate rows from this stager's own gate registers (run right
+        // after commit, before the next prefetch reuses them): the in-chunk
+        // cumulative log-gate in the wave's private row gcw (lane = token), and,
+        // from stager 0, the rows b = e^gc, w, gc and b_C, gc_C that the B-waves read.
+        auto gate_rows = [&](int ci) {
+            const int b = ci & 1;
+            float* G = sG(b);
+            float* gcw = reinterpret_cast<float*>(smem + Ly::GC_OFF) + 64 * wa;
+            const bool b16 = FAM == FAM_GDN && p.gate_bf16;
+            const float graw = __builtin_bit_cast(float, b16 ? pg << 16 : pg);
+            const float gate = lane < CH ? (FAM == FAM_GDN ? graw : Ah * graw) : 0.f;
+            const float gc = wave_incl_scan(gate);
+            const float gtot = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, gc), CH - 1));
+            gcw[lane] = gc;
+            if (wa == 0) {
+                if (lane < CH) {
+                    G[2 * CH + lane] = __expf(gc);
+                    const float wt = __expf(gtot - gc);
+                    G[3 * CH + lane] = (FAM == FAM_GDN) ? wt : graw * wt;
+                    G[4 * CH + lane] = gc;
                 }
-                const float gci = gcw[16 * mt + c16];
-                const f32x4 gt = lds4f(gcw + 16 * mt + 4 * g);
-                const f32x4 bt = lds4f(G + CH + 16 * mt + 4 * g);
-                f32x4 l;
-#pragma unroll
-                for (int r = 0; r < 4; ++r) l[r] = (c16 < 4 * g + r) ? bt[r] * __expf(gt[r] - gci) * acc[r] : 0.f;
-                // LTd[i][t] = L[t][i]
-                *reinterpret_cast<f32x4*>(INV + c16 * SLD + 4 * g) = l;
+                if (lane == 0) {
+                    G[5 * CH] = __expf(gtot);
+                    G[5 * CH + 1] = gtot;
+                }
+                lam_sum += gtot;
             }
         };
+
+        // Gated DeltaNet: (I + L_mm)^{-1} of the diagonal blocks.  The stagers put
+        // the masked diagonal blocks in LDS (diag_prep; stager a takes blocks
+        // NSTG-1-a, 2 NSTG-1-a, ...) and signal the solver through an LDS counter;
+        // the solver inverts them all at once by right-looking forward substitution
+        // with each block in registers, so the 16 dependent steps wait on FMAs only.
+        // A stager's blocks are formed together: every fragment and gate is
+        // requested first, then the blocks run as independent accumulation chains.
+        auto diag_prep = [&](auto first_c, int b, const float* gcw) {
+            constexpr int F = decltype(first_c)::value;
+            constexpr int NMY = F < NTC ? (NTC - F + NSTG - 1) / NSTG : 0;
+            if constexpr (FAM == FAM_GDN && NMY > 0) {
+                const float* G = sG(b);
+                auto krow = [&](int i) { return sK(b) + (16 * (F + i * NSTG) + c16) * SK; };
+                f32x4 acc[NMY], gt[NMY], bt[NMY];
+                float gci[NMY];
+#pragma unroll
+                for (int i = 0; i < NMY; ++i) acc[i] = zero4();
+                auto gates = [&]() {
+#pragma unroll
+                    for (int i = 0; i < NMY; ++i) {
+                        const int mt = F + i * NSTG;
+                        gci[i] = gcw[16 * mt + c16];
+                        gt[i] = lds4f(gcw + 16 * mt + 4 * g);
+                        bt[i] = lds4f(G + CH + 16 * mt + 4 * g);
+                    }
+                };
+                if constexpr (NK == 1) {
+#pragma unroll
+                    for (int i = 0; i < NMY; ++i) {
+                        const bf16* kr = krow(i);
+                        acc[i] = mma16(lds4(kr + 4 * g), lds4(kr + 4 * g), acc[i]);
+                        if (F32IO) {
+                            acc[i] = mma16(lds4(kr + 4 * g), lds4(kr + KPL + 4 * g), acc[i]);
+                            acc[i] = mma16(lds4(kr + KPL + 4 * g), lds4(kr + 4 * g), acc[i]);
+                        }
+                    }
+                    gates();
+                } else {
+                    constexpr int NKP = NK / 2;
+                    bf16x8 kv[NKP][NMY], lv[F32IO ? NKP : 1][NMY];
+#pragma unroll
+                    for (int kp = 0; kp < NKP; ++kp)
+#pragma unroll
+                        for (int i = 0; i < NMY; ++i) {
+                            kv[kp][i] = lds8(krow(i) + 32 * kp + 8 * g);
+                            if constexpr (F32IO) lv[kp][i] = lds8(krow(i) + KPL + 32 * kp + 8 * g);
+                        }
+                    gates();
+                    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                    for (int kp = 0; kp < NKP; ++kp)
+#pragma unroll
+                        for (int i = 0; i < NMY; ++i) {
+                            acc[i] = mma32(kv[kp][i], kv[kp][i], acc[i]);
+                            if constexpr (F32IO) {
+                                acc[i] = mma32(kv[kp][i], lv[kp][i], acc[i]);
+                                acc[i] = mma32(lv[kp][i], kv[kp][i], acc[i]);
+                            }
+                        }
+                }
+#pragma unroll
+                for (int i = 0; i < NMY; ++i) {
+                    float* INV = reinterpret_cast<float*>(smem + Ly::INV_OFF) + (F + i * NSTG) * Ly::INV_BST;
+                    f32x4 l;
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        l[r] = (c16 < 4 * g + r) ? bt[i][r] * __expf(gt[i][r] - gci[i]) * acc[i][r] : 0.f;
+                    // LTd[i][t] = L[t][i]
+                    *reinterpret_cast<f32x4*>(INV + c16 * SLD + 4 * g) = l;
+                }
+            }
+        };
+        uint32_t* diag_cnt = reinterpret_cast<uint32_t*>(smem + Ly::CNT_OFF);
         // One wave inverts every diagonal block: lane c of lane group g solves
         // column c of block g (the masked blocks were left in LDS by diag_prep).
         auto diag_solve_all = [&](int b) {
@@ -809,60 +873,55 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
             }
         };
 
-        // A-waves: state-independent blocks of chunk ci into buffer ci & 1
+        // A-waves, second phase: state-independent blocks of chunk ci into buffer ci & 1
         auto a_work = [&](int ci) {
             const int b = ci & 1;
-            float* G = sG(b);
-            float* gcw = reinterpret_cast<float*>(smem + Ly::GC_OFF) + 64 * wa;
-            // in-chunk cumulative log-gate, lane = token
-            const float gate = lane < CH ? (FAM == FAM_GDN ? G[lane] : Ah * G[lane]) : 0.f;
-            const float gc = wave_incl_scan(gate);
-            const float gtot = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, gc), CH - 1));
-            gcw[lane] = gc;
-            if (wa == 0) {
-                if (lane < CH) {
-                    G[2 * CH + lane] = __expf(gc);
-                    const float wt = __expf(gtot - gc);
-                    G[3 * CH + lane] = (FAM == FAM_GDN) ? wt : G[lane] * wt;
-                }
-                if (lane < CH) G[4 * CH + lane] = gc;
-                if (lane == 0) {
-                    G[5 * CH] = __expf(gtot);
-                    G[5 * CH + 1] = gtot;
-                }
-                lam_sum += gtot;
+            if (FAM == FAM_GDN && !stager) {
+                // the solver: wait until every stager has masked its diagonal blocks
+                // of chunk ci (NSTG signals per chunk), then invert them
+                lds_wait_count(diag_cnt, (uint32_t)(NSTG * (ci + 1)));
+                diag_solve_all(b);
+                return;
             }
-            wave_lds_sync();
+            // this wave's gate prefix row (gate_rows, one barrier earlier)
+            const float* gcw = reinterpret_cast<const float*>(smem + Ly::GC_OFF) + 64 * wa;
             if constexpr (FAM == FAM_GDN) {
-                if (stager) {
-                    // stager a builds the strictly-lower L blocks a, a + NSTG, ...
-                    using NS = integral_constant<int, NSTG>;
-                    switch (wa) {
-                        case 0: items(integral_constant<int, 0>(), NS(), L_KIND(), b, gcw); break;
-                        case 1: items(integral_constant<int, 1 % NSTG>(), NS(), L_KIND(), b, gcw); break;
-                        default: items(integral_constant<int, 2 % NSTG>(), NS(), L_KIND(), b, gcw); break;
-                    }
-                } else {
-                    // the solver masks every diagonal block, then inverts them all
-#pragma unroll
-                    for (int mt = 0; mt < NTC; ++mt) diag_prep(b, gcw, mt);
-                    wave_lds_sync();
-                    diag_solve_all(b);
+                // stager a masks its diagonal blocks and signals the solver, then
+                // builds the strictly-lower L blocks a, a + NSTG, ...
+                static_assert(NSTG == 3, "three stagers");
+                using NS = integral_constant<int, NSTG>;
+                switch (wa) {
+                    case 0:
+                        diag_prep(integral_constant<int, 2>(), b, gcw);
+                        lds_signal(diag_cnt, lane);
+                        items(integral_constant<int, 0>(), NS(), L_KIND(), b, gcw);
+                        break;
+                    case 1:
+                        diag_prep(integral_constant<int, 1>(), b, gcw);
+                        lds_signal(diag_cnt, lane);
+                        items(integral_constant<int, 1>(), NS(), L_KIND(), b, gcw);
+                        break;
+                    default:
+                        diag_prep(integral_constant<int, 0>(), b, gcw);
+                        lds_signal(diag_cnt, lane);
+                        items(integral_constant<int, 2>(), NS(), L_KIND(), b, gcw);
+                        break;
                 }
             }
         };
 
         // prologue: chunk 0 staged and its blocks built; chunk 1 in flight.  While
         // the B-waves run chunk c, the stagers commit chunk c+1 (loaded during
-        // chunk c-1), issue the loads of chunk c+2, and build chunk c+1's L
-        // blocks; the solver forms chunk c's T blocks, then masks and inverts
-        // chunk c+1's diagonal blocks.
+        // chunk c-1), issue the loads of chunk c+2, and mask chunk c+1's diagonal
+        // blocks and build its L blocks; the solver forms chunk c's T blocks, then
+        // inverts chunk c+1's diagonal blocks.
         // The stagers and the solver also run separate loops (same barrier
         // sequence), so the solver's registers do not overlap the prefetch ones.
         if (stager) {
             if (nch > 0) {
                 prefetch(0);
                 commit(0);
+                gate_rows(0);
             }
             chunk_barrier();
             if (nch > 0) {
@@ -871,7 +930,10 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
             }
             for (int ci = 0; ci < nch; ++ci) {
                 chunk_barrier();
-                if (ci + 1 < nch) commit(ci + 1);
+                if (ci + 1 < nch) {
+                    commit(ci + 1);
+                    gate_rows(ci + 1);
+                }
                 if (ci + 2 < nch) prefetch(ci + 2);  // a whole chunk of lead time
                 chunk_barrier();
                 if (ci + 1 < nch) a_work(ci + 1);

@@ -164,6 +164,26 @@ __device__ __forceinline__ void lds_barrier() {
 
 // Memory fence + instruction barrier for one wave's own LDS traffic: orders a
 // wave's LDS writes before its later LDS reads of other lanes' data.
+// Point-to-point signal between waves of one workgroup through an LDS counter,
+// for producers and a consumer inside one barrier interval.  lds_signal: after
+// this wave's earlier LDS writes have completed, lane 0 adds 1 (the LDS executes
+// its operations in order, so a wave that reads the new count and then reads
+// those locations sees the writes).  lds_wait_count: spins (with s_sleep) until
+// the count reaches `target`.  The spin is bounded (about 2^20 polls, tens of
+// milliseconds) so that a missing signal cannot keep the workgroup resident.
+__device__ __forceinline__ void lds_signal(uint32_t* cnt, int lane) {
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    if (lane == 0) __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+__device__ __forceinline__ void lds_wait_count(const uint32_t* cnt, uint32_t target) {
+    for (int spin = 0; spin < (1 << 20); ++spin) {
+        const uint32_t v = __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        if (__builtin_amdgcn_readfirstlane(v) >= target) break;
+        __builtin_amdgcn_s_sleep(1);
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+}
+
 __device__ __forceinline__ void wave_lds_sync() {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
