@@ -99,8 +99,9 @@ struct ChunkLds {
     static constexpr size_t K_SZ = al(size_t(PL) * CH * SK * 2);
     static constexpr size_t Q_SZ = HAS_Q ? al(size_t(PL) * CH * SK * 2) : 0;
     static constexpr size_t V_SZ = al(size_t(PL) * CH * SV * 2);
-    // gate rows: raw gate | beta | b | w | cumulative gate gc | b_C, gc_C
-    static constexpr size_t G_SZ = al((5 * CH + 4) * 4);
+    // gate rows: raw gate | beta | b | w | cumulative gate gc | b_C, gc_C (4) | beta b
+    static constexpr int BB_ROW = 5 * CH + 4;
+    static constexpr size_t G_SZ = al((6 * CH + 4) * 4);
     static constexpr size_t LT_SZ = HAS_L ? al(size_t(NOFF) * BLK * 2 * 2) : 0;
     static constexpr size_t NT_SZ = HAS_L ? al(size_t(NTC) * BLK * 2 * 2) : 0;
     static constexpr size_t PT_SZ = HAS_Q ? al(size_t(NPB) * BLK * PL * 2) : 0;
@@ -375,25 +376,36 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                     }
                 }
                 if (FAM == FAM_GDN) {
-                    // K S^T for all token tiles at once (interleaved chains, hi and lo passes apart)
-                    f32x4 kh[RT][NTC], kl[RT][NTC];
+                    // K S^T for all token tiles at once (interleaved chains, passes pass-major)
+                    f32x4 ks[RT][NTC];
 #pragma unroll
                     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-                        for (int mt = 0; mt < NTC; ++mt) kh[rt][mt] = kl[rt][mt] = zero4();
+                        for (int mt = 0; mt < NTC; ++mt) ks[rt][mt] = zero4();
                     if constexpr (RT == 1)
-                        mgemm_rows<NTC, F32IO, true>(Kb + c16 * SK, 16 * SK, KPL, Sh[0], Sl[0], NTK, g, kh[0], kl[0]);
+                        mgemm_rows<NTC, F32IO, true>(Kb + c16 * SK, 16 * SK, KPL, Sh[0], Sl[0], NTK, g, ks[0]);
                     else
-                        mgemm_rows_rt<NTC, RT, NTK, F32IO, true>(Kb + c16 * SK, 16 * SK, KPL, Sh, Sl, g, kh, kl);
+                        mgemm_rows_rt<NTC, RT, NTK, F32IO, true>(Kb + c16 * SK, 16 * SK, KPL, Sh, Sl, g, ks);
+                    // X = beta (v - b k S^T) = beta v - (beta b) k S^T  (v = 0 on transition tiles)
+                    if (load_v) {
 #pragma unroll
-                    for (int mt = 0; mt < NTC; ++mt) {
-                        const f32x4 bt = lds4f(G + 2 * CH + 16 * mt + 4 * g);
-                        const f32x4 be = lds4f(G + CH + 16 * mt + 4 * g);
+                        for (int mt = 0; mt < NTC; ++mt) {
+                            const f32x4 bb = lds4f(G + Ly::BB_ROW + 16 * mt + 4 * g);
+                            const f32x4 be = lds4f(G + CH + 16 * mt + 4 * g);
 #pragma unroll
-                        for (int rt = 0; rt < RT; ++rt) {
-                            const f32x4 ks = kh[rt][mt] + kl[rt][mt];
+                            for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-                            for (int r = 0; r < 4; ++r) X[rt][mt][r] = be[r] * (X[rt][mt][r] - bt[r] * ks[r]);
+                                for (int r = 0; r < 4; ++r)
+                                    X[rt][mt][r] = be[r] * X[rt][mt][r] - bb[r] * ks[rt][mt][r];
+                        }
+                    } else {
+#pragma unroll
+                        for (int mt = 0; mt < NTC; ++mt) {
+                            const f32x4 bb = lds4f(G + Ly::BB_ROW + 16 * mt + 4 * g);
+#pragma unroll
+                            for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                                for (int r = 0; r < 4; ++r) X[rt][mt][r] = -bb[r] * ks[rt][mt][r];
                         }
                     }
                 }
@@ -697,7 +709,7 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
         // Per-chunk gate rows from this stager's own gate registers (run right
         // after commit, before the next prefetch reuses them): the in-chunk
         // cumulative log-gate in the wave's private row gcw (lane = token), and,
-        // from stager 0, the rows b = e^gc, w, gc and b_C, gc_C that the B-waves read.
+        // from stager 0, the rows b = e^gc, w, gc, b_C, gc_C and beta b that the B-waves read.
         auto gate_rows = [&](int ci) {
             const int b = ci & 1;
             float* G = sG(b);
@@ -710,10 +722,12 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
             gcw[lane] = gc;
             if (wa == 0) {
                 if (lane < CH) {
-                    G[2 * CH + lane] = __expf(gc);
+                    const float bt = __expf(gc);
+                    G[2 * CH + lane] = bt;
                     const float wt = __expf(gtot - gc);
                     G[3 * CH + lane] = (FAM == FAM_GDN) ? wt : graw * wt;
                     G[4 * CH + lane] = gc;
+                    if (FAM == FAM_GDN) G[Ly::BB_ROW + lane] = __builtin_bit_cast(float, b16 ? pb << 16 : pb) * bt;
                 }
                 if (lane == 0) {
                     G[5 * CH] = __expf(gtot);

@@ -13,20 +13,23 @@ namespace lkv {
 // contraction slices outside and the tiles inside keeps NM independent chains
 // in flight.  nk = number of 16-slices (1, or even).
 
-// acc_h[m] += A_m x B (hi passes), acc_l[m] += lo passes, for NM tiles whose A
-// rows are LDS rows `a0 + m * mstep` of a K / Q tile in kq_pos order (this
-// lane's row, hi plane; lo plane at + plane), B = acc-layout register tiles.
+// acc[m] += A_m x B (all passes), for NM tiles whose A rows are LDS rows
+// `a0 + m * mstep` of a K / Q tile in kq_pos order (this lane's row, hi plane;
+// lo plane at + plane), B = acc-layout register tiles (hi bh, lo bl).  Within
+// each contraction slice the passes are issued pass-major (every tile's hi pass,
+// then every tile's lo passes), so consecutive products never share an
+// accumulator.
 template <int NM, bool ALO, bool BLO>
 __device__ __forceinline__ void mgemm_rows(const bf16* a0, int mstep, int plane, const bf16x4* bh,
-                                           const bf16x4* bl, int nk, int g, f32x4* acc_h, f32x4* acc_l) {
+                                           const bf16x4* bl, int nk, int g, f32x4* acc) {
     if (nk == 1) {
 #pragma unroll
         for (int m = 0; m < NM; ++m) {
             const bf16* ar = a0 + m * mstep + 4 * g;
             const bf16x4 x = lds4(ar);
-            acc_h[m] = mma16(x, bh[0], acc_h[m]);
-            if (BLO) acc_l[m] = mma16(x, bl[0], acc_l[m]);
-            if (ALO) acc_l[m] = mma16(lds4(ar + plane), bh[0], acc_l[m]);
+            acc[m] = mma16(x, bh[0], acc[m]);
+            if (BLO) acc[m] = mma16(x, bl[0], acc[m]);
+            if (ALO) acc[m] = mma16(lds4(ar + plane), bh[0], acc[m]);
         }
         return;
     }
@@ -49,21 +52,24 @@ __device__ __forceinline__ void mgemm_rows(const bf16* a0, int mstep, int plane,
     for (int kp = 0; kp < NP; ++kp) {
         if (2 * kp >= nk) break;
 #pragma unroll
-        for (int m = 0; m < NM; ++m) {
-            acc_h[m] = mma32(xh[kp][m], bh[2 * kp], bh[2 * kp + 1], acc_h[m]);
-            if (BLO) acc_l[m] = mma32(xh[kp][m], bl[2 * kp], bl[2 * kp + 1], acc_l[m]);
-            if constexpr (ALO) acc_l[m] = mma32(xl[kp][m], bh[2 * kp], bh[2 * kp + 1], acc_l[m]);
+        for (int m = 0; m < NM; ++m) acc[m] = mma32(xh[kp][m], bh[2 * kp], bh[2 * kp + 1], acc[m]);
+        if (BLO) {
+#pragma unroll
+            for (int m = 0; m < NM; ++m) acc[m] = mma32(xh[kp][m], bl[2 * kp], bl[2 * kp + 1], acc[m]);
+        }
+        if constexpr (ALO) {
+#pragma unroll
+            for (int m = 0; m < NM; ++m) acc[m] = mma32(xl[kp][m], bh[2 * kp], bh[2 * kp + 1], acc[m]);
         }
     }
 }
 
 // mgemm_rows for RT independent right-hand sides B_rt (the state row tiles of
-// one wave) sharing every A fragment: acc_h[rt][m] += A_m x B_rt (hi passes),
-// acc_l[rt][m] += lo passes.  nk = NTK 16-slices (even, at least 2).
+// one wave) sharing every A fragment: acc[rt][m] += A_m x B_rt (all passes,
+// pass-major).  nk = NTK 16-slices (even, at least 2).
 template <int NM, int RT, int NTK, bool ALO, bool BLO>
 __device__ __forceinline__ void mgemm_rows_rt(const bf16* a0, int mstep, int plane, const bf16x4 (&bh)[RT][NTK],
-                                              const bf16x4 (&bl)[RT][NTK], int g, f32x4 (&acc_h)[RT][NM],
-                                              f32x4 (&acc_l)[RT][NM]) {
+                                              const bf16x4 (&bl)[RT][NTK], int g, f32x4 (&acc)[RT][NM]) {
     static_assert(NTK % 2 == 0, "32-wide slices");
     constexpr int NP = NTK / 2;
 #pragma unroll
@@ -79,11 +85,22 @@ __device__ __forceinline__ void mgemm_rows_rt(const bf16* a0, int mstep, int pla
 #pragma unroll
         for (int m = 0; m < NM; ++m)
 #pragma unroll
-            for (int rt = 0; rt < RT; ++rt) {
-                acc_h[rt][m] = mma32(xh[m], bh[rt][2 * kp], bh[rt][2 * kp + 1], acc_h[rt][m]);
-                if (BLO) acc_l[rt][m] = mma32(xh[m], bl[rt][2 * kp], bl[rt][2 * kp + 1], acc_l[rt][m]);
-                if constexpr (ALO) acc_l[rt][m] = mma32(xl[m], bh[rt][2 * kp], bh[rt][2 * kp + 1], acc_l[rt][m]);
-            }
+            for (int rt = 0; rt < RT; ++rt)
+                acc[rt][m] = mma32(xh[m], bh[rt][2 * kp], bh[rt][2 * kp + 1], acc[rt][m]);
+        if (BLO) {
+#pragma unroll
+            for (int m = 0; m < NM; ++m)
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt)
+                    acc[rt][m] = mma32(xh[m], bl[rt][2 * kp], bl[rt][2 * kp + 1], acc[rt][m]);
+        }
+        if constexpr (ALO) {
+#pragma unroll
+            for (int m = 0; m < NM; ++m)
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt)
+                    acc[rt][m] = mma32(xl[m], bh[rt][2 * kp], bh[rt][2 * kp + 1], acc[rt][m]);
+        }
     }
 }
 
