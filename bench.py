@@ -471,8 +471,9 @@ def main():
 
         pick = {"scan": lambda n: chunk_mode(n) == (fam, False),
                 "fold": lambda n: chunk_mode(n) == (fam, True),
-                "compose": lambda n: "compose" in n,
-                "init_single": lambda n: "init_single" in n}
+                # the step composes from and copies out of fp32 pools (the <..., false> variants)
+                "compose": lambda n: "compose" in n and n.rstrip(">").endswith("false"),
+                "init_single": lambda n: "init_single" in n and n.rstrip(">").endswith("false")}
         for op, pred in pick.items():
             cand = [v for (n, grid), v in table.items() if pred(n)]
             if len(cand) == 1:
