@@ -313,3 +313,39 @@ def test_ssd_lambda_only(case):
     got = _np(lam)
     assert np.max(np.abs(got - ref) / np.maximum(np.abs(ref), 1e-30)) < STATE_TOL
     assert np.max(np.abs(got - _np(G.M_pool)) / np.maximum(np.abs(ref), 1e-30)) < STATE_TOL
+
+
+# The method's degenerate gates, on the online scan:
+#   Gated DeltaNet alpha = 1, beta = 0: every update term is an exact zero and
+#   b_C = 1, so the state passes through bit for bit and o = scale * S_0 q;
+#   alpha = 1, beta = 1 (the plain delta rule); strong forgetting (log alpha = -30
+#   per token, so a chunk's decay underflows); Mamba-2 with vanishing dt and
+#   with dt = 4 (per-token decay e^-4 .. e^-16; larger dt would only grow the
+#   outputs past what bf16 rounding keeps within the absolute output bar).
+DEGENERATE = [
+    (I.GDN, 0.0, 0.0, True),
+    (I.GDN, 0.0, 1.0, False),
+    (I.GDN, -30.0, 0.5, False),
+    (I.SSD, 1e-6, None, False),
+    (I.SSD, 4.0, None, False),
+]
+
+
+@pytest.mark.parametrize("fam,gate,beta,identity", DEGENERATE,
+                         ids=["gdn_a1_b0", "gdn_a1_b1", "gdn_forget", "ssd_dt_tiny", "ssd_dt_large"])
+def test_degenerate_gates(fam, gate, beta, identity):
+    case = (64, 64, 64, "bf16", 2, 2, ((130, 64), (1,), (40,)), (150, 64, 1)) if fam == I.GDN \
+        else (128, 64, 64, "bf16", 1, 4, ((130, 64), (1,), (40,)), (150, 64, 1))
+    w = _work(fam, case)
+    w.online.g[...] = gate
+    if beta is not None:
+        w.online.beta[...] = beta
+    rng = np.random.default_rng(5)
+    L = w.layer
+    S0 = (0.5 * rng.standard_normal((w.n_req, L.h_v, L.dv, L.dk))).astype(np.float32)
+    G = gpu_io.GpuWorkload(w, with_cached=False)
+    if identity:
+        G.scan(_dev(S0))
+        torch.cuda.synchronize()
+        assert np.array_equal(_np(G.S_final).view(np.uint32), S0.view(np.uint32))
+    _scan_check(w, G, S0)
