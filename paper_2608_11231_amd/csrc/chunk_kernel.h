@@ -364,8 +364,10 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                             if (F32IO) X[rt][mt] += to_f32(lds4_tr(sV(b) + VPL, SV, 16 * mt, col, g, c16));
                         }
                     }
-                if (with_out) {
-                    // this chunk's output blocks P, shared by the B-waves (read after the barrier)
+                if (FAM == FAM_GDN && with_out) {
+                    // Gated DeltaNet: this chunk's output blocks P, shared by the B-waves
+                    // (read after the barrier).  The stagers' second phase is full with
+                    // the L blocks; Mamba-2's stagers build P instead.
                     using NS = integral_constant<int, NB>;
                     const float* gcp = G + 4 * CH;
                     switch (w) {
@@ -899,11 +901,11 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
             }
             // this wave's gate prefix row (gate_rows, one barrier earlier)
             const float* gcw = reinterpret_cast<const float*>(smem + Ly::GC_OFF) + 64 * wa;
+            using NS = integral_constant<int, NSTG>;
             if constexpr (FAM == FAM_GDN) {
                 // stager a masks its diagonal blocks and signals the solver, then
                 // builds the strictly-lower L blocks a, a + NSTG, ...
                 static_assert(NSTG == 3, "three stagers");
-                using NS = integral_constant<int, NSTG>;
                 switch (wa) {
                     case 0:
                         diag_prep(integral_constant<int, 2>(), b, gcw);
@@ -921,14 +923,24 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                         items(integral_constant<int, 2>(), NS(), L_KIND(), b, gcw);
                         break;
                 }
+            } else if (with_out) {
+                // Mamba-2: stager a builds the output blocks P a, a + NSTG, ... (these
+                // waves are otherwise idle in this phase)
+                static_assert(NSTG == 4, "four stagers");
+                switch (wa) {
+                    case 0: items(integral_constant<int, 0>(), NS(), P_KIND(), b, gcw); break;
+                    case 1: items(integral_constant<int, 1>(), NS(), P_KIND(), b, gcw); break;
+                    case 2: items(integral_constant<int, 2>(), NS(), P_KIND(), b, gcw); break;
+                    default: items(integral_constant<int, 3>(), NS(), P_KIND(), b, gcw); break;
+                }
             }
         };
 
         // prologue: chunk 0 staged and its blocks built; chunk 1 in flight.  While
         // the B-waves run chunk c, the stagers commit chunk c+1 (loaded during
         // chunk c-1), issue the loads of chunk c+2, and mask chunk c+1's diagonal
-        // blocks and build its L blocks; the solver forms chunk c's T blocks, then
-        // inverts chunk c+1's diagonal blocks.
+        // blocks and build its L blocks (Mamba-2: its P blocks); the solver forms
+        // chunk c's T blocks, then inverts chunk c+1's diagonal blocks.
         // The stagers and the solver also run separate loops (same barrier
         // sequence), so the solver's registers do not overlap the prefetch ones.
         if (stager) {
