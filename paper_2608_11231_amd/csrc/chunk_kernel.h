@@ -22,17 +22,21 @@
 // token x token products and masks, inverses of the 16x16 diagonal blocks of
 // I + L) and the state chain.  The workgroup runs them as a two-stage
 // software pipeline over chunks:
-//   * A-waves (NA = 4): stage chunk c+1 from registers into LDS and prefetch
-//     chunk c+2 from HBM; then compute chunk c+1's state-independent blocks,
-//     stored pre-split (bf16 hi/lo) and transposed for direct fragment reads:
-//     the strictly-lower L blocks and the inverses of the 16x16 diagonal blocks
-//     of I + L.  For Gated DeltaNet one A-wave does not stage: it masks and
-//     inverts chunk c+1's diagonal blocks, and while the B-waves start chunk c
-//     it combines chunk c's inverses into the off-diagonal blocks of the two
-//     32x32 diagonal blocks of (I + L)^{-1};
-//   * B-waves (NB, 16 state rows each): chunk c's state chain -- K S^T, the
-//     two-level block substitution for U (32-token halves), the outputs, the
-//     state update -- with the fp32 state held in MFMA accumulator registers.
+//   * A-waves (NA = 4).  The stagers (3 for Gated DeltaNet, 4 for Mamba-2)
+//     commit chunk c+1 from registers into LDS, form its gate prefix from
+//     their own gate registers and prefetch chunk c+2 from HBM (first phase);
+//     then they build chunk c+1's state-independent blocks, stored pre-split
+//     (bf16 hi/lo) and transposed for direct fragment reads (second phase):
+//     Gated DeltaNet's masked diagonal blocks of L (handed to the solver
+//     through an LDS signal count) and strictly-lower L blocks, or Mamba-2's
+//     output blocks P.  Gated DeltaNet's fourth A-wave, the solver, inverts
+//     chunk c+1's diagonal blocks (second phase) and combines chunk c's
+//     inverses into the off-diagonal blocks of the two 32x32 diagonal blocks
+//     of (I + L)^{-1} while the B-waves start chunk c (first phase);
+//   * B-waves (NB, 16*RT state rows each): chunk c's state chain -- K S^T (and
+//     Gated DeltaNet's output blocks P), the two-level block substitution for
+//     U (32-token halves), the outputs, the state update -- with the fp32
+//     state held in MFMA accumulator registers.
 // LDS holds two pipeline buffers; two workgroup barriers per chunk.  In the
 // block summary the barriers order LDS traffic only (prefetched loads stay in
 // flight across them); the scan keeps full barriers, which measured faster.

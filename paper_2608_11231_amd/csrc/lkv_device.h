@@ -169,14 +169,16 @@ __device__ __forceinline__ void lds_barrier() {
 // this wave's earlier LDS writes have completed, lane 0 adds 1 (the LDS executes
 // its operations in order, so a wave that reads the new count and then reads
 // those locations sees the writes).  lds_wait_count: spins (with s_sleep) until
-// the count reaches `target`.  The spin is bounded (about 2^20 polls, tens of
-// milliseconds) so that a missing signal cannot keep the workgroup resident.
+// the count reaches `target`.  A legitimate wait is a fraction of a chunk (well
+// under 200 polls); the spin is bounded at 2^14 polls (about a millisecond) so that
+// a missing signal ends in wrong values within milliseconds, never in a
+// workgroup that stays resident.
 __device__ __forceinline__ void lds_signal(uint32_t* cnt, int lane) {
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     if (lane == 0) __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 __device__ __forceinline__ void lds_wait_count(const uint32_t* cnt, uint32_t target) {
-    for (int spin = 0; spin < (1 << 20); ++spin) {
+    for (int spin = 0; spin < (1 << 14); ++spin) {
         const uint32_t v = __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
         if (__builtin_amdgcn_readfirstlane(v) >= target) break;
         __builtin_amdgcn_s_sleep(1);
