@@ -4,8 +4,9 @@
 One step is one pass of the whole hot path over one batch of synthetic input
 already resident in HBM:
   1. lkv_init_single   -- LinearKV's single-block initial state (last block),
-  2. lkv_block_summary -- online fold of every cached block's transition M_k
-                          (the exact-composition mode's extra work),
+  2. lkv_block_summary -- online fold of the cached blocks' transitions M_k that
+                          the composition reads (blocks 2..K of each request;
+                          the exact-composition mode's extra work),
   3. lkv_init_compose  -- exact composition of the K cached (M_k, B_k) pairs,
   4. the chunk scan    -- Gated DeltaNet (or Mamba-2) recurrence over the online
                           tokens from the composed state, with outputs.
@@ -78,17 +79,20 @@ def work_model(w):
         per_chunk = 2 * C * C * dk + 2 * C * C * dv + 2 * 2 * C * dk * dv
     out["scan"] = dict(bytes=T * (2 * hq * dk * io + hv * dv * io * 2 + n_gates * hv * gb) + 2 * state,
                        flops=chunks * hv * per_chunk)
-    # fold (transitions of every cached block)
-    if L.family == 0:
-        cchunks = sum(-(-int(x) // C) for x in np.diff(w.cached.cu))
-        per = 2 * C * C * dk + C ** 3 / 3 + 2 * C * dk * dk + 2 * C * C * dk + 2 * C * dk * dk
-        out["fold"] = dict(bytes=Tc * (hq * dk * io + 2 * hv * gb) + n_blk * hv * dk * dk * 4,
-                           flops=cchunks * hv * per)
-    else:
-        out["fold"] = dict(bytes=Tc * hv * 4 + n_blk * hv * 4, flops=Tc * hv)
-    # composition
+    # fold: the transitions the composition reads, blocks 2..K of each request
     K = np.diff(w.blk_cu)
     n_trans = int(np.sum(np.maximum(K - 1, 0)))
+    first = {int(w.blk_ids[w.blk_cu[r]]) for r in range(n_req) if K[r] > 0}
+    blens = [int(x) for b, x in enumerate(np.diff(w.cached.cu)) if b not in first]
+    Tf = sum(blens)
+    if L.family == 0:
+        cchunks = sum(-(-x // C) for x in blens)
+        per = 2 * C * C * dk + C ** 3 / 3 + 2 * C * dk * dk + 2 * C * C * dk + 2 * C * dk * dk
+        out["fold"] = dict(bytes=Tf * (hq * dk * io + 2 * hv * gb) + n_trans * hv * dk * dk * 4,
+                           flops=cchunks * hv * per)
+    else:
+        out["fold"] = dict(bytes=Tf * hv * 4 + n_trans * hv * 4, flops=Tf * hv)
+    # composition
     if L.family == 0:
         out["compose"] = dict(bytes=(n_blk * hv * dv * dk + n_trans * hv * dk * dk) * 4 + state,
                               flops=n_trans * hv * 2 * dv * dk * dk)
@@ -269,7 +273,7 @@ def diag_bench(w, G, steps: int):
         lkv.gdn_chunk_scan(G.layer, full, 1.0, None, None, S_star)
     else:
         lkv.ssd_chunk_scan(G.layer, full, None, None, S_star)
-    G.block_summary(B=False, M=True)
+    G.fold_transitions()
     G.init_single()
     G.init_compose()
     h = w.layer.h_v
@@ -315,12 +319,13 @@ def cpu_baseline(w, budget_s: float):
     else:
         oracle.ssd_scan(cu, o.q[s0:s1], o.k[s0:s1], o.v[s0:s1], o.g[s0:s1], w.A, S0=S0)
     t_scan = time.perf_counter() - tic
-    # fold sample: request 0's blocks, as many as fit in the remaining budget
+    # fold sample: request 0's blocks 2..K (the transitions the composition reads),
+    # as many as fit in the remaining budget
     fold_blocks = []
     est_per_tok = t_scan / max(s1 - s0, 1)
     room = max(budget_s - 2 * t_scan, budget_s * 0.25)
     tok = 0
-    for b in range(b0, b1):
+    for b in range(b0 + 1 if b1 > b0 + 1 else b0, b1):
         L_b = int(c.cu[b + 1] - c.cu[b])
         if fold_blocks and (tok + L_b) * est_per_tok > room:
             break
@@ -351,7 +356,9 @@ def cpu_baseline(w, budget_s: float):
     # scale each op to the whole batch by its units of work
     T_all = w.online.n_tok
     n_trans_all = int(np.sum(np.maximum(np.diff(w.blk_cu) - 1, 0)))
-    step = (t_scan * T_all / (s1 - s0) + t_fold * w.cached.n_tok / (ft1 - ft0)
+    first = {int(w.blk_ids[w.blk_cu[r]]) for r in range(w.n_req) if w.blk_cu[r + 1] > w.blk_cu[r]}
+    T_fold = sum(int(x) for b, x in enumerate(np.diff(c.cu)) if b not in first)
+    step = (t_scan * T_all / (s1 - s0) + t_fold * T_fold / max(ft1 - ft0, 1)
             + t_comp * n_trans_all / max(K0 - 1, 1) + t_single * w.n_req)
     sample = (f"request 0 of {w.n_req}, all {L.h_v} heads: scan of {s1 - s0} online tokens "
               f"({t_scan:.2f} s), transition fold of {len(fold_blocks)} cached blocks / {ft1 - ft0} tokens "
@@ -396,7 +403,7 @@ def main():
     log("[bench] inputs resident in HBM; block states built")
 
     ops = [("init_single", G.init_single),
-           ("fold", lambda: G.block_summary(B=False, M=True)),
+           ("fold", G.fold_transitions),
            ("compose", G.init_compose),
            ("scan", lambda: G.scan(G.S_exact))]
 

@@ -75,6 +75,31 @@ class GpuWorkload:
         lkv.block_summary(self.layer, self.cached.struct, self.B_pool if B else None,
                           self.M_pool if M else None, stream)
 
+    def fold_view(self) -> "GpuTokens":
+        """The cached stream as the composition's transition fold needs it: the
+        composition never reads a request's first block's transition (Eq. 6
+        starts from that block's state), so each request's first block is an
+        empty segment (its M_pool row becomes the identity, or Lambda = 0) and
+        only blocks 2..K keep their k / gate rows.  Pool row b stays segment b."""
+        if getattr(self, "_fold_view", None) is None:
+            w, c = self.w, self.w.cached
+            first = sorted({int(w.blk_ids[w.blk_cu[r]]) for r in range(w.n_req)
+                            if w.blk_cu[r + 1] > w.blk_cu[r]})
+            lens = np.diff(c.cu).astype(np.int64)
+            keep = np.ones(c.n_tok, bool)
+            for b in first:
+                keep[c.cu[b]:c.cu[b + 1]] = False
+                lens[b] = 0
+            cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+            tok = I.Tokens(cu, None, c.k[keep], None, c.g[keep], None if c.beta is None else c.beta[keep])
+            self._fold_view = GpuTokens(tok, w.layer, w.A, with_q=False)
+        return self._fold_view
+
+    def fold_transitions(self, stream=None):
+        """The transitions M_k (Lambda_k) of blocks 2..K of every request, as the
+        exact composition reads them (the online fold of exact composition)."""
+        lkv.block_summary(self.layer, self.fold_view().struct, None, self.M_pool, stream)
+
     def init_single(self, stream=None):
         lkv.init_single(self.layer, self.w.n_blk, self.B_pool, self.last_blk, self.S_single, stream)
 

@@ -90,12 +90,29 @@ def test_full_size_config(index, mild):
     S1, SX, SF, out = _np(G.S_single), _np(G.S_exact), _np(G.S_final), _np(G.out)
     # the benchmark's fold asks for the transitions only (Mamba-2: the segmented dt sum)
     G.block_summary(B=False, M=True)
+    G.init_compose()
     torch.cuda.synchronize()
-    M_only = _np(G.M_pool)
+    M_only, SX_only = _np(G.M_pool), _np(G.S_exact)
     if L.family == I.GDN:
         assert np.array_equal(M_only.view(np.uint32), M_pool.view(np.uint32))
     else:
         assert np.max(np.abs(M_only - M_pool) / np.maximum(np.abs(M_pool), 1e-30)) < 1e-5
+    # ... over blocks 2..K only (each request's first block an empty segment): the
+    # same transitions bit for bit, identity (Lambda = 0) rows for the first
+    # blocks, and the same composed state, bit for bit
+    G.fold_transitions()
+    G.init_compose()
+    torch.cuda.synchronize()
+    M_fold, SX_fold = _np(G.M_pool), _np(G.S_exact)
+    first = sorted({int(w.blk_ids[w.blk_cu[r]]) for r in range(w.n_req) if w.blk_cu[r + 1] > w.blk_cu[r]})
+    rest = [b for b in range(w.n_blk) if b not in first]
+    assert np.array_equal(M_fold[rest].view(np.uint32), M_only[rest].view(np.uint32))
+    if L.family == I.GDN:
+        eye = np.broadcast_to(np.eye(L.dk, dtype=np.float32), M_fold[first].shape)
+        assert np.array_equal(M_fold[first], eye)
+    else:
+        assert np.all(M_fold[first] == 0)
+    assert np.array_equal(SX_fold.view(np.uint32), SX_only.view(np.uint32))
     # the single-block state is a bit-exact copy of the pool row
     assert np.array_equal(S1.view(np.uint32), B_pool[w.last_blk].view(np.uint32))
     rng = np.random.default_rng(index)
