@@ -58,6 +58,9 @@ CASES = [
     (I.GDN, 32, 48, "bf16", 2, 4, (130, 77, 300, 50, 0, 64)),
     (I.GDN, 16, 16, "f32", 1, 1, (33, 20, 5, 9)),
     (I.SSD, 64, 32, "bf16", 2, 4, (150, 41, 90, 12)),
+    # more requests than a workgroup has threads: the request search takes two
+    # passes and reads the offsets past the first 256 from global memory
+    (I.GDN, 16, 16, "bf16", 1, 2, tuple((7 * r + 3) % 13 for r in range(300))),
 ]
 
 
