@@ -170,15 +170,26 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
         if (tid == 0) *reinterpret_cast<uint32_t*>(smem + Ly::CNT_OFF) = 0u;
     }
 
-    // ---- work unit
+    // ---- work unit.  Order of the units, innermost first: the row tiles and the
+    // value heads of one q/k head (they read the same token rows, so they share
+    // an L2), then hpx = h_qk / 8 adjacent q/k heads (neighbouring row segments
+    // of the same tokens, read at the same time), then the segment, then the
+    // group of hpx q/k heads.  xcd_unit hands each XCD a contiguous range, i.e.
+    // one head group of every segment: ragged segment lengths then load the
+    // XCDs evenly (giving each XCD whole segments left the fold 13% unbalanced
+    // at 32K and the ragged batch 50%).
     const int tiles = p.tiles_b + p.tiles_m;
+    const int hr = p.h_v / p.h_qk;  // value heads per q/k head
+    const int hpx = (p.h_qk % 8 == 0) ? p.h_qk / 8 : 1;
     const int u = xcd_unit(blockIdx.x, p.n_units);
-    const int tile = u % tiles;
-    const int h = (u / tiles) % p.h_v;
-    const int s = u / (tiles * p.h_v);
+    const int inner = u % (tiles * hr), outer = u / (tiles * hr);
+    const int tile = inner % tiles;
+    const int hsub = outer % hpx, o2 = outer / hpx;
+    const int s = o2 % p.n_seq;
+    const int hq = (o2 / p.n_seq) * hpx + hsub;
+    const int h = hq * hr + inner / tiles;
     const bool mtile = tile >= p.tiles_b;
     const int row0 = (mtile ? tile - p.tiles_b : tile) * 16 * NB * RT;  // first state row of the tile
-    const int hq = h / (p.h_v / p.h_qk);
     int64_t t0 = p.cu[s], t1 = p.cu[s + 1];
     t0 = t0 < 0 ? 0 : (t0 > p.n_tok ? p.n_tok : t0);
     t1 = t1 < t0 ? t0 : (t1 > p.n_tok ? p.n_tok : t1);

@@ -195,10 +195,14 @@ __global__ __launch_bounds__(64 * NW) void compose_gdn_kernel(ComposeArgs p) {
     bf16* sMl = sMh + DK * SM;
     const int tid = threadIdx.x;
     const int w = tid >> 6, lane = tid & 63, g = lane >> 4, c16 = lane & 15;
+    // units: the row tiles of one (request, head) adjacent, then the request
+    // index fastest, so each XCD's range holds a few heads of every request
+    // (ragged block counts load the XCDs evenly)
     const int u = xcd_unit(blockIdx.x, p.n_units);
+    const int n_req = p.n_units / (p.tiles * p.h_v);
     const int tile = u % p.tiles;
-    const int h = (u / p.tiles) % p.h_v;
-    const int r = u / (p.tiles * p.h_v);
+    const int r = (u / p.tiles) % n_req;
+    const int h = u / (p.tiles * n_req);
     const int my_row = tile * 16 * NW + 16 * w + c16;
 
     int32_t b0 = p.blk_cu[r], b1 = p.blk_cu[r + 1];

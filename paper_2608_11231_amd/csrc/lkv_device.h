@@ -148,8 +148,9 @@ __device__ __forceinline__ float wave_incl_scan(float x) {
 
 // Workgroup -> work-unit map that gives each XCD a contiguous range of units.
 // The hardware deals workgroups round-robin over the 8 XCDs (b % 8); units
-// that are adjacent in the caller's order (same head, same request) then share
-// one XCD's L2.  The map is a bijection on [0, n).
+// that are adjacent in the caller's order then share one XCD's L2 (callers
+// order their units so that adjacent ones read the same rows).  The map is a
+// bijection on [0, n).
 __device__ __forceinline__ int xcd_unit(int b, int n) {
     const int q = n >> 3, r = n & 7, x = b & 7, i = b >> 3;
     return x * q + min(x, r) + i;
