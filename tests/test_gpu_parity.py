@@ -42,6 +42,8 @@ GDN_CASES = [
     (128, 128, 64, "bf16", 2, 2, ((200, 77),), (193,)),
     (64, 64, 64, "f32", 1, 2, ((90,), (65, 3)), (129, 0)),
     (64, 48, 16, "bf16", 1, 1, ((33,),), (47,)),
+    # the largest supported state (dk = 128, dv = 512): eight row tiles per head
+    (128, 512, 64, "bf16", 1, 2, ((70, 33),), (90,)),
 ]
 
 SSD_CASES = [
@@ -50,6 +52,7 @@ SSD_CASES = [
     (128, 64, 64, "bf16", 1, 4, ((130, 64), (1, 70)), (150, 64)),
     (64, 32, 16, "bf16", 2, 4, ((50,),), (77,)),
     (64, 64, 16, "f32", 1, 2, ((20,),), (33,)),
+    (128, 512, 64, "bf16", 1, 2, ((70,),), (90,)),
 ]
 
 
@@ -111,7 +114,7 @@ def _orth_pool(rng, n, h, d, scale=0.9):
     return (scale * q).reshape(n, h, d, d)
 
 
-@pytest.mark.parametrize("dk,dv", [(16, 16), (64, 48), (128, 128)])
+@pytest.mark.parametrize("dk,dv", [(16, 16), (64, 48), (128, 128), (128, 512)])
 def test_gdn_compose_o1_transitions(dk, dv):
     """Composition on O(1)-norm transitions (0.9 x orthogonal), so every block matters."""
     rng = np.random.default_rng(dk + dv)
