@@ -44,7 +44,7 @@
 extern "C" {
 #endif
 
-#define LKV_ABI_VERSION 6
+#define LKV_ABI_VERSION 7
 
 typedef enum {
     LKV_OK = 0,
@@ -111,6 +111,22 @@ const char* lkv_status_string(lkv_status s);
 
 /* hipError_t behind the last LKV_E_HIP returned on the calling thread. */
 int lkv_last_hip_error(void);
+
+/* Bound of the chunk kernels' one inter-wave wait.  Within a workgroup of the
+ * Gated DeltaNet chunk kernels (lkv_block_summary, lkv_gdn_chunk_scan,
+ * lkv_chunk_scan_from_pool), one wave inverts the diagonal blocks of
+ * (I + diag(beta) strictly-lower(K K^T)) -- the delta rule's triangular system
+ * of the chunkwise form of Eq. 3 -- after the waves that mask them signal
+ * through a counter in LDS.  That wait polls the counter at most `polls` times
+ * (with a short sleep between polls).  A wait that gives up stores NaN blocks,
+ * so the chunk's state rows and outputs, and every later chunk's, become NaN:
+ * a missed signal is visible in the results, never silently wrong, and every
+ * kernel still ends.  The default, 16384 polls, is about a millisecond, against
+ * well under 200 polls for a legitimate wait; 0 never polls, so every wait
+ * gives up (a host-forced failure for tests); a negative value restores the
+ * default.  Process-wide; read by each call when it launches.  Returns the
+ * previous bound. */
+int32_t lkv_set_wait_limit(int32_t polls);
 
 /* Per-block summary (Eq. 5): for every segment of `blocks`, scanned from an
  * empty start, write

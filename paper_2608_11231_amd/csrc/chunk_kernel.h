@@ -81,6 +81,7 @@ struct ScanArgs {
     int32_t tiles_m;      // row tiles over dk (transition rows), GDN summary only
     int32_t nb;           // B-waves per workgroup (16*nb rows per tile)
     int32_t n_units;
+    int32_t wait_limit;   // polls of the solver's bounded wait for the stagers' signals
 };
 
 template <int FAM, int DK, int CH, bool F32IO, int NB, bool SUMMARY>
@@ -829,7 +830,9 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
         uint32_t* diag_cnt = reinterpret_cast<uint32_t*>(smem + Ly::CNT_OFF);
         // One wave inverts every diagonal block: lane c of lane group g solves
         // column c of block g (the masked blocks were left in LDS by diag_prep).
-        auto diag_solve_all = [&](int b) {
+        // A wait that gave up (ok false) stores NaN blocks: the chunk's state and
+        // outputs then become NaN instead of values built from stale LDS.
+        auto diag_solve_all = [&](int b, bool ok) {
             if constexpr (FAM == FAM_GDN) {
                 if (g < NTC) {
                     const float* LTd = reinterpret_cast<const float*>(smem + Ly::INV_OFF) + g * Ly::INV_BST;
@@ -848,6 +851,10 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
 #pragma unroll
                             for (int i = m + 1; i < 16; ++i) a[i] += Lc[m][i >> 2][i & 3] * x[m];
                         }
+                    }
+                    if (!ok) {
+#pragma unroll
+                        for (int m = 0; m < 16; ++m) x[m] = __builtin_nanf("");
                     }
                     // NT[c][m] = N[m][c]: this lane's column is one contiguous NT row
                     bf16* nt_hi = sNT(b) + g * BLK + c16 * SB;
@@ -910,8 +917,8 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
             if (FAM == FAM_GDN && !stager) {
                 // the solver: wait until every stager has masked its diagonal blocks
                 // of chunk ci (NSTG signals per chunk), then invert them
-                lds_wait_count(diag_cnt, (uint32_t)(NSTG * (ci + 1)));
-                diag_solve_all(b);
+                const bool ok = lds_wait_count(diag_cnt, (uint32_t)(NSTG * (ci + 1)), p.wait_limit);
+                diag_solve_all(b, ok);
                 return;
             }
             // this wave's gate prefix row (gate_rows, one barrier earlier)

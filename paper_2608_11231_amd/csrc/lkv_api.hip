@@ -2,6 +2,8 @@
 // launch-geometry selection and dispatch to the gfx950 kernels.
 #include <stdlib.h>
 
+#include <atomic>
+
 #include "decode_kernels.h"
 #include "diag_kernels.h"
 #include "gather_kernels.h"
@@ -15,6 +17,9 @@ using namespace lkv;
 namespace {
 
 thread_local int g_last_hip = 0;
+// polls of the chunk kernels' bounded stager -> solver wait (lkv_set_wait_limit)
+constexpr int32_t kDefaultWaitLimit = 1 << 14;
+std::atomic<int32_t> g_wait_limit{kDefaultWaitLimit};
 
 lkv_status hip_status(hipError_t e) {
     if (e == hipSuccess) return LKV_OK;
@@ -101,6 +106,7 @@ ScanArgs base_args(const lkv_layer* L, const lkv_tokens* T) {
     a.dv = L->dv;
     a.gate_bf16 = L->gate_dtype == LKV_BF16;
     a.scale = 1.f;
+    a.wait_limit = g_wait_limit.load(std::memory_order_relaxed);
     return a;
 }
 
@@ -242,6 +248,11 @@ const char* lkv_status_string(lkv_status s) {
 }
 
 int lkv_last_hip_error(void) { return g_last_hip; }
+
+int32_t lkv_set_wait_limit(int32_t polls) {
+    if (polls < 0) polls = kDefaultWaitLimit;
+    return g_wait_limit.exchange(polls, std::memory_order_relaxed);
+}
 
 lkv_status lkv_block_summary(const lkv_layer* L, const lkv_tokens* T, float* B_out, float* M_out,
                              void* stream) {

@@ -169,22 +169,29 @@ __device__ __forceinline__ void lds_barrier() {
 // for producers and a consumer inside one barrier interval.  lds_signal: after
 // this wave's earlier LDS writes have completed, lane 0 adds 1 (the LDS executes
 // its operations in order, so a wave that reads the new count and then reads
-// those locations sees the writes).  lds_wait_count: spins (with s_sleep) until
-// the count reaches `target`.  A legitimate wait is a fraction of a chunk (well
-// under 200 polls); the spin is bounded at 2^14 polls (about a millisecond) so that
-// a missing signal ends in wrong values within milliseconds, never in a
-// workgroup that stays resident.
+// those locations sees the writes).  lds_wait_count: polls (with s_sleep) until
+// the count reaches `target`, at most `limit` times, and returns whether it did.
+// A legitimate wait is a fraction of a chunk (well under 200 polls); the default
+// bound of 2^14 polls (about a millisecond) makes a missing signal end the wait
+// within milliseconds, never in a workgroup that stays resident.  The caller
+// turns a wait that gave up into NaN results; limit 0 never polls and always
+// gives up.
 __device__ __forceinline__ void lds_signal(uint32_t* cnt, int lane) {
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     if (lane == 0) __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
-__device__ __forceinline__ void lds_wait_count(const uint32_t* cnt, uint32_t target) {
-    for (int spin = 0; spin < (1 << 14); ++spin) {
+__device__ __forceinline__ bool lds_wait_count(const uint32_t* cnt, uint32_t target, int limit) {
+    bool reached = false;
+    for (int spin = 0; spin < limit; ++spin) {
         const uint32_t v = __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-        if (__builtin_amdgcn_readfirstlane(v) >= target) break;
+        if (__builtin_amdgcn_readfirstlane(v) >= target) {
+            reached = true;
+            break;
+        }
         __builtin_amdgcn_s_sleep(1);
     }
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    return reached;
 }
 
 __device__ __forceinline__ void wave_lds_sync() {

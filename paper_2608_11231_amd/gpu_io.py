@@ -27,6 +27,15 @@ def _t(x: Optional[np.ndarray], dtype, device) -> Optional[torch.Tensor]:
     return torch.from_numpy(np.ascontiguousarray(x)).to(device=device, dtype=dtype)
 
 
+def fold_dropped_blocks(w: I.Workload):
+    """Pool rows whose transition no composition of ``w`` reads: every block that
+    is not at position 2..K of some request."""
+    read = set()
+    for r in range(w.n_req):
+        read.update(int(b) for b in w.blk_ids[w.blk_cu[r] + 1:w.blk_cu[r + 1]])
+    return sorted(set(range(w.n_blk)) - read)
+
+
 class GpuTokens:
     """A token stream resident in HBM plus its C struct."""
 
@@ -76,18 +85,21 @@ class GpuWorkload:
                           self.M_pool if M else None, stream)
 
     def fold_view(self) -> "GpuTokens":
-        """The cached stream as the composition's transition fold needs it: the
-        composition never reads a request's first block's transition (Eq. 6
-        starts from that block's state), so each request's first block is an
-        empty segment (its M_pool row becomes the identity, or Lambda = 0) and
-        only blocks 2..K keep their k / gate rows.  Pool row b stays segment b."""
+        """The cached stream as the composition's transition fold needs it.  The
+        composition never reads the transition of a request's first block (Eq. 6
+        starts from that block's state), so a block whose transition no request
+        reads -- one that is only ever some request's first block, or is in no
+        request at all -- becomes an empty segment (its M_pool row turns into the
+        identity, or Lambda = 0).  A block that is first in one request and a
+        later block of another keeps its rows: position-independent caching
+        reuses one cached block in any position (Sec. 3.2).  Pool row b stays
+        segment b."""
         if getattr(self, "_fold_view", None) is None:
             w, c = self.w, self.w.cached
-            first = sorted({int(w.blk_ids[w.blk_cu[r]]) for r in range(w.n_req)
-                            if w.blk_cu[r + 1] > w.blk_cu[r]})
+            drop = fold_dropped_blocks(w)
             lens = np.diff(c.cu).astype(np.int64)
             keep = np.ones(c.n_tok, bool)
-            for b in first:
+            for b in drop:
                 keep[c.cu[b]:c.cu[b + 1]] = False
                 lens[b] = 0
             cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)

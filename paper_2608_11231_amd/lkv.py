@@ -51,7 +51,7 @@ EXPORTS = ("lkv_abi_version", "lkv_status_string", "lkv_last_hip_error", "lkv_bl
            "lkv_init_single", "lkv_init_compose", "lkv_gdn_chunk_scan", "lkv_ssd_chunk_scan",
            "lkv_gdn_decode", "lkv_ssd_decode", "lkv_gather_selected", "lkv_init_single_bf16",
            "lkv_init_compose_bf16", "lkv_round_bf16", "lkv_stage_rows", "lkv_state_rel_error",
-           "lkv_chunk_scan_from_pool")
+           "lkv_chunk_scan_from_pool", "lkv_set_wait_limit")
 
 
 def load() -> ctypes.CDLL:
@@ -69,6 +69,8 @@ def load() -> ctypes.CDLL:
             lib.lkv_status_string.restype = ctypes.c_char_p
             lib.lkv_status_string.argtypes = [ctypes.c_int]
             lib.lkv_last_hip_error.restype = ctypes.c_int
+            lib.lkv_set_wait_limit.argtypes = [i32]
+            lib.lkv_set_wait_limit.restype = i32
             lib.lkv_block_summary.argtypes = [LP, TP, vp, vp, vp]
             lib.lkv_init_single.argtypes = [LP, i32, i32, vp, vp, vp, vp]
             lib.lkv_init_compose.argtypes = [LP, i32, i32, vp, vp, vp, vp, i32, vp, vp]
@@ -255,3 +257,10 @@ def chunk_scan_from_pool(layer: Layer, online: Tokens, scale: float, B_pool: Opt
     _check(load().lkv_chunk_scan_from_pool(ctypes.byref(layer), ctypes.byref(online), float(scale), _ptr(B_pool), dt,
                                            int(n_blk), _ptr(src_blk), _ptr(out), _ptr(S_final), _stream(stream)),
            "lkv_chunk_scan_from_pool")
+
+
+def set_wait_limit(polls: int) -> int:
+    """Bound of the chunk kernels' stager-to-solver wait (polls; 0 = always give
+    up, negative = the default).  A wait that gives up makes the results NaN.
+    Returns the previous bound."""
+    return int(load().lkv_set_wait_limit(int(polls)))

@@ -37,9 +37,20 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_strings(lib):
-    assert lib.lkv_abi_version() == 6
+    assert lib.lkv_abi_version() == 7
     assert lib.lkv_status_string(0) == b"ok"
     assert b"NULL" in lib.lkv_status_string(1)
+
+
+def test_wait_limit_setter(lib):
+    """The bound of the chunk kernels' inter-wave wait is host state: the setter
+    returns the previous bound, and a negative value restores the default."""
+    default = lib.lkv_set_wait_limit(-1)
+    assert default == 1 << 14
+    assert lib.lkv_set_wait_limit(0) == default
+    assert lib.lkv_set_wait_limit(5) == 0
+    assert lib.lkv_set_wait_limit(-3) == 5
+    assert lib.lkv_set_wait_limit(-1) == default
 
 
 def _layer(**kw):

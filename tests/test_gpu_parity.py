@@ -352,3 +352,129 @@ def test_degenerate_gates(fam, gate, beta, identity):
         torch.cuda.synchronize()
         assert np.array_equal(_np(G.S_final).view(np.uint32), S0.view(np.uint32))
     _scan_check(w, G, S0)
+
+
+@pytest.mark.parametrize("chunk", [16, 64])
+def test_wait_that_gives_up_makes_nan(chunk):
+    """The solver's bounded wait, forced from the host to give up at once (0
+    polls): every Gated DeltaNet chunk kernel still ends, its states,
+    transitions and outputs come out NaN on every non-empty segment instead of
+    plausible values, and with the default bound back the same calls match the
+    oracle again."""
+    case = (64, 64, chunk, "bf16", 2, 2, ((130, 64), (0, 9), (5,)), (150, 0, 64))
+    w = _work(I.GDN, case)
+    G = gpu_io.GpuWorkload(w)
+    G.block_summary()                      # a valid pool for the scan from the pool
+    torch.cuda.synchronize()
+    pool = _np(G.B_pool)
+    prev = lkv.set_wait_limit(0)
+    try:
+        G.scan(None)
+        lkv.chunk_scan_from_pool(G.layer, G.online.struct, w.scale, G.B_pool, w.n_blk, G.last_blk, G.out,
+                                 G.S_exact)
+        G.block_summary()
+        torch.cuda.synchronize()
+    finally:
+        lkv.set_wait_limit(prev)
+    blens = np.diff(w.cached.cu)
+    olens = np.diff(w.online.cu)
+    B, M = _np(G.B_pool), _np(G.M_pool)
+    for b, n in enumerate(blens):
+        assert np.isnan(B[b]).all() == (n > 0) and np.isnan(M[b]).all() == (n > 0), b
+        if n == 0:
+            assert np.array_equal(B[b], np.zeros_like(B[b]))
+            assert np.array_equal(M[b], np.broadcast_to(np.eye(w.layer.dk, dtype=np.float32), M[b].shape))
+    SF, SP = _np(G.S_final), _np(G.S_exact)
+    for r, n in enumerate(olens):
+        assert np.isnan(SF[r]).all() == (n > 0) and np.isnan(SP[r]).all() == (n > 0), r
+        if n == 0:
+            assert np.array_equal(SF[r], np.zeros_like(SF[r]))
+            assert np.array_equal(SP[r].view(np.uint32), pool[w.last_blk[r]].view(np.uint32))
+    assert np.isnan(_np(G.out)).all()
+    # default bound restored: normal results
+    G.block_summary()
+    G.scan(None)
+    torch.cuda.synchronize()
+    Bo, Mo = R.summaries(w)
+    assert rel_slices(_np(G.B_pool), Bo) < STATE_TOL and rel_slices(_np(G.M_pool), Mo) < STATE_TOL
+    o_ref, S_ref = R.scan(w, None)
+    assert rel_slices(_np(G.S_final), S_ref) < STATE_TOL
+    assert max_abs(_np(G.out), o_ref) < OUT_ABS
+
+
+@pytest.mark.parametrize("scale", [0.9, 0.99])
+def test_gdn_compose_32_blocks(scale):
+    """Exact composition at the 32K workload's depth and width (K = 32 chained
+    products, dk = dv = 128) on O(1)-norm transitions (scale x orthogonal), so
+    every block contributes; shorter requests (K = 16, 8, 4, 2) reuse pool rows
+    in other orders.  The error per K is printed for the design notes."""
+    rng = np.random.default_rng(3200)
+    n_blk, h, d = 40, 4, 128
+    B = rng.standard_normal((n_blk, h, d, d)).astype(np.float32)
+    M = _orth_pool(rng, n_blk, h, d, scale).astype(np.float32)
+    Ks = [32, 16, 8, 4, 2]
+    ids = np.concatenate([rng.permutation(n_blk)[:k] for k in Ks]).astype(np.int32)
+    blk_cu = np.concatenate([[0], np.cumsum(Ks)]).astype(np.int32)
+    layer = lkv.make_layer(I.GDN, 1, h, d, d, 64)
+    S = torch.empty((len(Ks), h, d, d), device="cuda")
+    lkv.init_compose(layer, n_blk, _dev(B), _dev(M), torch.from_numpy(ids).cuda(),
+                     torch.from_numpy(blk_cu).cuda(), len(ids), S)
+    torch.cuda.synchronize()
+    import oracle
+    ref = oracle.compose_gdn(blk_cu, ids, B, M)
+    got = _np(S)
+    errs = {k: rel_slices(got[[r]], ref[[r]]) for r, k in enumerate(Ks)}
+    print(f"compose K-chain error at scale {scale}: " + ", ".join(f"K={k} {e:.2e}" for k, e in errs.items()))
+    assert max(errs.values()) < STATE_TOL, errs
+
+
+@pytest.mark.parametrize("nb", [1, 2, 4, 8])
+@pytest.mark.parametrize("fam", [I.GDN, I.SSD])
+def test_dv512_pinned_geometry(fam, nb, monkeypatch):
+    """The largest state (dk = 128, dv = 512) in every launch geometry the chunk
+    kernels have: 16 nb state rows per workgroup (nb = 8: four waves of two row
+    tiles, block summaries only), i.e. 32 / nb row tiles per head; the scan takes
+    nb up to 4 (eight row tiles per head at dv = 512)."""
+    case = GDN_CASES[-1] if fam == I.GDN else SSD_CASES[-1]
+    w = _work(fam, case)
+    G = gpu_io.GpuWorkload(w)
+    monkeypatch.setenv("LKV_SCAN_NB", str(nb))
+    G.block_summary()
+    torch.cuda.synchronize()
+    B, M = R.summaries(w)
+    assert rel_slices(_np(G.B_pool), B) < STATE_TOL
+    if fam == I.GDN:
+        assert rel_slices(_np(G.M_pool), M) < STATE_TOL
+    else:
+        assert np.max(np.abs(_np(G.M_pool) - M) / np.maximum(np.abs(M), 1e-30)) < STATE_TOL
+    monkeypatch.setenv("LKV_SCAN_NB", str(min(nb, 4)))
+    S0 = R.init_compose(w, B, M)
+    _scan_check(w, gpu_io.GpuWorkload(w, with_cached=False), S0)
+
+
+def test_fold_view_keeps_blocks_reused_later():
+    """Position-independent caching reuses a cached block in any position: a
+    block that is one request's first block and a later block of another keeps
+    its transition in the fold over blocks 2..K; only blocks whose transition
+    no request reads are emptied.  The composed states match the oracle."""
+    import dataclasses
+    w = _work(I.GDN, (64, 64, 64, "bf16", 2, 2, ((70, 90, 40), (130, 20)), (64, 80)))
+    # pool rows 0..4; request 0 = [0, 1, 2], request 1 = [3, 4], request 2 = [2, 0, 4]
+    ids = np.array([0, 1, 2, 3, 4, 2, 0, 4], np.int32)
+    blk_cu = np.array([0, 3, 5, 8], np.int32)
+    w = dataclasses.replace(w, blk_ids=ids, blk_cu=blk_cu, last_blk=np.array([2, 4, 4], np.int32),
+                            online=w.online.__class__(np.array([0, 64, 100, 144], np.int32),
+                                                      *[None if a is None else a[:144] for a in
+                                                        (w.online.q, w.online.k, w.online.v, w.online.g,
+                                                         w.online.beta)]))
+    assert gpu_io.fold_dropped_blocks(w) == [3]
+    G = gpu_io.GpuWorkload(w)
+    G.block_summary(B=True, M=False)
+    G.fold_transitions()
+    G.init_compose()
+    torch.cuda.synchronize()
+    B, M = R.summaries(w)
+    got_M = _np(G.M_pool)
+    assert rel_slices(got_M[[0, 1, 2, 4]], M[[0, 1, 2, 4]]) < STATE_TOL
+    assert np.array_equal(got_M[3], np.broadcast_to(np.eye(64, dtype=np.float32), got_M[3].shape))
+    assert rel_slices(_np(G.S_exact), R.init_compose(w, B, M)) < STATE_TOL
