@@ -13,10 +13,16 @@ already resident in HBM:
 The per-block states B_k are the cache's content (computed offline in the
 paper), so they are built once before timing.
 
-Prints ONE JSON line.  ``value`` = online tokens / step time.  Per-kernel
-durations come from HIP events on the stream the library launches on, inside
-the timed region; ``roofline`` is given for the kernel that takes the most time
-and ``roofline_by_kernel`` for all four.  ``cpu_baseline`` times the CPU oracle
+Prints ONE JSON line.  ``value`` = online tokens / step time, the step time
+being the median over the timed steps, each run cold: an untimed write of a
+512 MiB buffer before every step evicts the 256 MB Infinity Cache (warm,
+back-to-back figures are reported alongside).  Per-kernel durations come from
+HIP events on the stream the library launches on, inside the timed steps;
+``roofline`` is given for the kernel that takes the most time and
+``roofline_by_kernel`` for all four, against the published peaks and against
+the peaks measured in the same run (``measured_peaks``: a 512 MiB device copy
+and a large bf16 matrix product).  ``other_workloads`` holds the same figures
+for the 8K Gated DeltaNet, 8K Mamba-2 and ragged 16K workloads.  ``cpu_baseline`` times the CPU oracle
 on a bounded sample of the same workload and scales it to the whole step.
 ``lb_fused_*`` times LinearKV's path as a single launch (the scan reading its
 initial state straight from the cached pool row).  ``decode_step`` times, after
@@ -27,7 +33,8 @@ online stream from the cached context at selected positions;
 ``bf16_pool_staging`` times the cache's bf16 storage path (pool rounding,
 host-to-device staging of a batch's rows, overlap with the scan);
 ``relative_error_probe`` gives both initial states' relative error against the
-full-prefix state and times the diagnostic kernel.
+full-prefix state, at the workload's gates and at slowly decaying gates (where
+every cached block contributes), and times the diagnostic kernel.
 """
 import argparse
 import json
@@ -48,6 +55,11 @@ RIDGE = MFMA_BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
+
+
+def fold_dropped_blocks(w):
+    from paper_2608_11231_amd.gpu_io import fold_dropped_blocks as f
+    return f(w)
 
 
 # ---------------------------------------------------------------- algorithmic work
@@ -71,27 +83,31 @@ def work_model(w):
     n_gates = 2 if L.family == 0 else 1
     out = {}
     out["init_single"] = dict(bytes=2 * state, flops=0)
-    # scan
-    chunks = sum(-(-int(x) // C) for x in np.diff(w.online.cu))
+    # scan: every chunk at its actual token count (a ragged tail chunk is not padded)
+    def chunk_sizes(lens):
+        for n in lens:
+            n = int(n)
+            for c0 in range(0, n, C):
+                yield min(C, n - c0)
     if L.family == 0:
-        per_chunk = 5 * 2 * C * C * dk + 3 * 2 * C * dk * dv + C ** 3 / 3
+        scan_flops = sum(5 * 2 * n * n * dk + 3 * 2 * n * dk * dv + n ** 3 / 3 for n in chunk_sizes(np.diff(w.online.cu)))
     else:
-        per_chunk = 2 * C * C * dk + 2 * C * C * dv + 2 * 2 * C * dk * dv
+        scan_flops = sum(2 * n * n * dk + 2 * n * n * dv + 2 * 2 * n * dk * dv for n in chunk_sizes(np.diff(w.online.cu)))
     out["scan"] = dict(bytes=T * (2 * hq * dk * io + hv * dv * io * 2 + n_gates * hv * gb) + 2 * state,
-                       flops=chunks * hv * per_chunk)
-    # fold: the transitions the composition reads, blocks 2..K of each request
+                       flops=scan_flops * hv)
+    # fold: the transitions the composition reads (blocks at position 2..K of some request)
     K = np.diff(w.blk_cu)
     n_trans = int(np.sum(np.maximum(K - 1, 0)))
-    first = {int(w.blk_ids[w.blk_cu[r]]) for r in range(n_req) if K[r] > 0}
-    blens = [int(x) for b, x in enumerate(np.diff(w.cached.cu)) if b not in first]
+    dropped = set(fold_dropped_blocks(w))
+    blens = [int(x) for b, x in enumerate(np.diff(w.cached.cu)) if b not in dropped]
     Tf = sum(blens)
     if L.family == 0:
-        cchunks = sum(-(-x // C) for x in blens)
-        per = 2 * C * C * dk + C ** 3 / 3 + 2 * C * dk * dk + 2 * C * C * dk + 2 * C * dk * dk
-        out["fold"] = dict(bytes=Tf * (hq * dk * io + 2 * hv * gb) + n_trans * hv * dk * dk * 4,
-                           flops=cchunks * hv * per)
+        fold_flops = sum(2 * n * n * dk + n ** 3 / 3 + 2 * n * dk * dk + 2 * n * n * dk + 2 * n * dk * dk
+                         for n in chunk_sizes(blens))
+        out["fold"] = dict(bytes=Tf * (hq * dk * io + 2 * hv * gb) + (w.n_blk - len(dropped)) * hv * dk * dk * 4,
+                           flops=fold_flops * hv)
     else:
-        out["fold"] = dict(bytes=Tf * hv * 4 + n_trans * hv * 4, flops=Tf * hv)
+        out["fold"] = dict(bytes=Tf * hv * 4 + (w.n_blk - len(dropped)) * hv * 4, flops=Tf * hv)
     # composition
     if L.family == 0:
         out["compose"] = dict(bytes=(n_blk * hv * dv * dk + n_trans * hv * dk * dk) * 4 + state,
@@ -102,19 +118,24 @@ def work_model(w):
     return out
 
 
-def roofline(name, work, ms):
+def roofline(name, work, ms, bound=None):
+    """Achieved rate of one kernel against its roofline.  ``bound`` defaults to the
+    side with the larger lower bound on time (bytes / HBM peak vs flops / bf16
+    MFMA peak); both fractions are given."""
     secs = ms * 1e-3
-    ai = work["flops"] / max(work["bytes"], 1)
-    if ai > RIDGE:
-        ach = work["flops"] / secs / 1e12
-        return dict(kernel=name, bound="mfma", achieved=round(ach, 2), peak=MFMA_BF16_PEAK_TFLOPS,
-                    unit="TFLOP/s", frac=round(ach / MFMA_BF16_PEAK_TFLOPS, 4), traffic=None,
-                    avg_us=round(ms * 1e3, 2), algorithmic_flops=work["flops"],
-                    algorithmic_bytes=work["bytes"])
-    ach = work["bytes"] / secs / 1e9
-    return dict(kernel=name, bound="hbm", achieved=round(ach, 1), peak=HBM_PEAK_GBS, unit="GB/s",
-                frac=round(ach / HBM_PEAK_GBS, 4), traffic=None, avg_us=round(ms * 1e3, 2),
-                algorithmic_flops=work["flops"], algorithmic_bytes=work["bytes"])
+    gbs = work["bytes"] / secs / 1e9
+    tfs = work["flops"] / secs / 1e12
+    if bound is None:
+        bound = "mfma" if work["flops"] / MFMA_BF16_PEAK_TFLOPS / 1e12 > work["bytes"] / HBM_PEAK_GBS / 1e9 \
+            else "hbm"
+    common = dict(traffic=None, avg_us=round(ms * 1e3, 2), algorithmic_flops=work["flops"],
+                  algorithmic_bytes=work["bytes"], frac_hbm=round(gbs / HBM_PEAK_GBS, 4),
+                  frac_mfma=round(tfs / MFMA_BF16_PEAK_TFLOPS, 4))
+    if bound == "mfma":
+        return dict(kernel=name, bound="mfma", achieved=round(tfs, 2), peak=MFMA_BF16_PEAK_TFLOPS,
+                    unit="TFLOP/s", frac=round(tfs / MFMA_BF16_PEAK_TFLOPS, 4), **common)
+    return dict(kernel=name, bound="hbm", achieved=round(gbs, 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                frac=round(gbs / HBM_PEAK_GBS, 4), **common)
 
 
 # ---------------------------------------------------------------- decode step
@@ -163,9 +184,11 @@ def decode_bench(w, S_final, steps: int, batches=(None, 256)):
 def gather_bench(w, G, steps: int):
     """Time the gather that forms the recompute's online stream from the context:
     each request's cached context (its blocks, in order) and as many uniformly
-    selected positions as it has online tokens.  The context's q is not part of
-    the cached stream; its k buffer stands in as the q source (same shape and
-    dtype).  Algorithmic bytes = every gathered row read once and written once."""
+    selected positions as it has online tokens.  The context's q rows are not
+    part of the cached stream; a separate seeded buffer of the same shape and
+    dtype is their source, so no row of one array is served from the cache by
+    the read of another.  Algorithmic bytes = every gathered row read once and
+    written once."""
     import torch
     from paper_2608_11231_amd import gpu_io
     from paper_2608_11231_amd import inputs as I
@@ -178,7 +201,9 @@ def gather_bench(w, G, steps: int):
         m = int(w.online.cu[r + 1] - w.online.cu[r])
         per.append(I.select_uniform(rng, n_ctx, m / n_ctx) if n_ctx else np.zeros(0, np.int32))
     sel_cu, pos = I.pack_selection(per)
-    sel = gpu_io.GpuSelection(G.cached, ctx_cu, sel_cu, pos, L, ctx_q=G.cached.k)
+    gen = torch.Generator(device="cuda").manual_seed(2608)
+    ctx_q = torch.randn(tuple(G.cached.k.shape), generator=gen, device="cuda").to(G.cached.k.dtype)
+    sel = gpu_io.GpuSelection(G.cached, ctx_cu, sel_cu, pos, L, ctx_q=ctx_q)
     for _ in range(3):
         sel.gather()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -288,9 +313,9 @@ def diag_bench(w, G, steps: int):
     torch.cuda.synchronize()
     us = e0.elapsed_time(e1) * 1e3 / steps
     nbytes = 2 * G.S_single.numel() * 4
-    log(f"[bench] layer-0 probe: exact {rx.max().item():.2e}, last block {r1.min().item():.3f}.."
-        f"{r1.max().item():.3f}; diagnostic {us:.2f} us")
-    return dict(rel_exact_vs_full_prefix=[float(x) for x in rx.cpu()],
+    log(f"[bench] layer-0 probe ({w.name}): exact {rx.max().item():.2e}, last block "
+        f"{r1.min().item():.3e}..{r1.max().item():.3e}; diagnostic {us:.2f} us")
+    return dict(workload=w.name, rel_exact_vs_full_prefix=[float(x) for x in rx.cpu()],
                 rel_last_block_vs_full_prefix=[float(x) for x in r1.cpu()],
                 kernel_us=round(us, 2), algorithmic_bytes=nbytes,
                 achieved_GBs=round(nbytes / us / 1e3, 1))
@@ -356,8 +381,8 @@ def cpu_baseline(w, budget_s: float):
     # scale each op to the whole batch by its units of work
     T_all = w.online.n_tok
     n_trans_all = int(np.sum(np.maximum(np.diff(w.blk_cu) - 1, 0)))
-    first = {int(w.blk_ids[w.blk_cu[r]]) for r in range(w.n_req) if w.blk_cu[r + 1] > w.blk_cu[r]}
-    T_fold = sum(int(x) for b, x in enumerate(np.diff(c.cu)) if b not in first)
+    dropped = set(fold_dropped_blocks(w))
+    T_fold = sum(int(x) for b, x in enumerate(np.diff(c.cu)) if b not in dropped)
     step = (t_scan * T_all / (s1 - s0) + t_fold * T_fold / max(ft1 - ft0, 1)
             + t_comp * n_trans_all / max(K0 - 1, 1) + t_single * w.n_req)
     sample = (f"request 0 of {w.n_req}, all {L.h_v} heads: scan of {s1 - s0} online tokens "
@@ -368,18 +393,180 @@ def cpu_baseline(w, budget_s: float):
                 step_s_extrapolated=round(step, 3))
 
 
+# ---------------------------------------------------------------- timing
+FLUSH_BYTES = 512 << 20   # twice the 256 MB Infinity Cache
+
+
+class Timer:
+    """Per-step and per-op HIP-event timing of a step made of ops, on the stream
+    the library launches on (torch's current stream).  Cold steps are each
+    preceded by an untimed write of a 512 MiB buffer, which evicts the Infinity
+    Cache; warm steps run back to back."""
+
+    def __init__(self):
+        import torch
+        self.torch = torch
+        self.flush_buf = torch.empty(FLUSH_BYTES // 4, dtype=torch.int32, device="cuda")
+
+    def flush(self, k):
+        self.flush_buf.fill_(k & 0x7fffffff)
+
+    def run(self, ops, steps: int, cold: bool):
+        torch = self.torch
+        ev = lambda: torch.cuda.Event(enable_timing=True)
+        marks = [[ev() for _ in range(len(ops) + 1)] for _ in range(steps)]
+        torch.cuda.synchronize()
+        for k in range(steps):
+            if cold:
+                self.flush(k)
+            m = marks[k]
+            m[0].record()
+            for i, (_, f) in enumerate(ops):
+                f()
+                m[i + 1].record()
+        torch.cuda.synchronize()
+        step_ms = [m[0].elapsed_time(m[-1]) for m in marks]
+        op_ms = {name: [m[i].elapsed_time(m[i + 1]) for m in marks] for i, (name, _) in enumerate(ops)}
+        return step_ms, op_ms
+
+
+def stats(xs):
+    xs = sorted(xs)
+    n = len(xs)
+    med = xs[n // 2] if n % 2 else 0.5 * (xs[n // 2 - 1] + xs[n // 2])
+    return dict(median_us=round(med * 1e3, 2), mean_us=round(sum(xs) / n * 1e3, 2), min_us=round(xs[0] * 1e3, 2),
+                max_us=round(xs[-1] * 1e3, 2), n=n)
+
+
+def measured_peaks():
+    """Measured denominators on this GPU, each the best median (of 20 launches)
+    over a few probes: HBM from plain device copies (read + write bytes / time)
+    of 512 MiB and 2 GiB and an in-place fp32 scale of 2 GiB; bf16 matrix-core
+    rate from torch.matmul (hipBLASLt) at 8192^3 and 16384 x 16384 x 8192."""
+    import torch
+
+    def med20(fn):
+        for _ in range(3):
+            fn()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(20)]
+        torch.cuda.synchronize()
+        for e0, e1 in evs:
+            e0.record()
+            fn()
+            e1.record()
+        torch.cuda.synchronize()
+        return sorted(e0.elapsed_time(e1) for e0, e1 in evs)[10] * 1e-3
+
+    hbm, mfma = {}, {}
+    for nbytes in (512 << 20, 2 << 30):
+        src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        hbm[f"copy_{nbytes >> 20}MiB"] = 2 * nbytes / med20(lambda: dst.copy_(src)) / 1e9
+        del src, dst
+    x = torch.ones((2 << 30) // 4, dtype=torch.float32, device="cuda")
+    hbm["scale_2048MiB"] = 2 * x.numel() * 4 / med20(lambda: x.mul_(1.0)) / 1e9
+    del x
+    for m_, n_, k_ in ((8192, 8192, 8192), (16384, 16384, 8192)):
+        a = torch.randn((m_, k_), device="cuda").to(torch.bfloat16)
+        b = torch.randn((k_, n_), device="cuda").to(torch.bfloat16)
+        mfma[f"matmul_{m_}x{n_}x{k_}"] = 2 * m_ * n_ * k_ / med20(lambda: torch.matmul(a, b)) / 1e12
+        del a, b
+    torch.cuda.empty_cache()
+    return dict(hbm_GBs=round(max(hbm.values()), 1), bf16_TFLOPs=round(max(mfma.values()), 1),
+                hbm_probes={k: round(v, 1) for k, v in hbm.items()},
+                mfma_probes={k: round(v, 1) for k, v in mfma.items()})
+
+
+def traffic_table(w):
+    """Measured HBM bytes per launch of each op of the step, from the committed
+    rocprofv3 counter summary of this workload, when it was taken on the current
+    kernel sources."""
+    from paper_2608_11231_amd import rocprof_summary
+    table = rocprof_summary.read_traffic(os.path.join(ROOT, "profiles", f"{w.name}_hbm_traffic.txt"))
+    if not table:
+        return {}
+    fam = w.layer.family
+
+    def chunk_mode(n):
+        # lkv::chunk_kernel<FAM,DK,CH,F32IO,NB,SUMMARY,RT>: family and summary flag
+        if not n.startswith("lkv::chunk_kernel<"):
+            return None
+        args = n[len("lkv::chunk_kernel<"):].rstrip(">").split(",")
+        return (int(args[0]), args[5] == "true") if len(args) >= 6 else None
+
+    pick = {"scan": lambda n: chunk_mode(n) == (fam, False),
+            "fold": (lambda n: chunk_mode(n) == (fam, True)) if fam == 0 else (lambda n: "ssd_lambda" in n),
+            # the step composes from and copies out of fp32 pools (the <..., false> variants)
+            "compose": lambda n: "compose" in n and n.rstrip(">").endswith("false"),
+            "init_single": lambda n: "init_single" in n and n.rstrip(">").endswith("false")}
+    out = {}
+    for op, pred in pick.items():
+        cand = [v for (n, grid), v in table.items() if pred(n)]
+        if len(cand) == 1:
+            out[op] = round(cand[0])
+    return out
+
+
+def measure(w, G, steps: int, warmup: int, timer: Timer):
+    """The step's four calls on workload ``w``: cold (the headline: Infinity Cache
+    flushed before every step, medians) and warm (back to back).  Returns the
+    per-op and per-step figures, the rooflines and the two paths' rates."""
+    ops = [("init_single", G.init_single),
+           ("fold", G.fold_transitions),
+           ("compose", G.init_compose),
+           ("scan", lambda: G.scan(G.S_exact))]
+    timer.run(ops, warmup, cold=False)
+    cold_step, cold_op = timer.run(ops, steps, cold=True)
+    warm_step, warm_op = timer.run(ops, steps, cold=False)
+    T = w.online.n_tok
+    cold = {k: stats(v) for k, v in cold_op.items()}
+    warm = {k: stats(v) for k, v in warm_op.items()}
+    med = {k: v["median_us"] * 1e-3 for k, v in cold.items()}   # ms
+    work = work_model(w)
+    # the Gated DeltaNet fold sits at the ridge (404 GFLOP over 1.32 GB at 32K) and its
+    # time goes to matrix-core work (the hi/lo passes double it): priced against MFMA
+    bounds = {"fold": "mfma"} if w.layer.family == 0 else {}
+    roofs = {name: roofline(name, work[name], med[name], bounds.get(name)) for name in med}
+    for op, tb in traffic_table(w).items():
+        roofs[op]["traffic"] = tb
+    step_med = stats(cold_step)["median_us"] * 1e-3
+    return dict(
+        step_cold=stats(cold_step), step_warm=stats(warm_step), ops_cold=cold, ops_warm=warm,
+        roofline_by_kernel=roofs, dominant=max(med, key=med.get),
+        tokens_per_s=round(T / (step_med * 1e-3), 1),
+        lb_tokens_per_s=round(T / ((med["init_single"] + med["scan"]) * 1e-3), 1),
+        ex_tokens_per_s=round(T / ((med["fold"] + med["compose"] + med["scan"]) * 1e-3), 1),
+        composition_latency_us=round(med["compose"] * 1e3, 2),
+        fold_plus_compose_latency_us=round((med["fold"] + med["compose"]) * 1e3, 2),
+        single_init_latency_us=round(med["init_single"] * 1e3, 2),
+        scan_us=round(med["scan"] * 1e3, 2))
+
+
+def workload_desc(w):
+    from paper_2608_11231_amd import inputs as I
+    L = w.layer
+    T = w.online.n_tok
+    return (f"{w.name}: {'Gated DeltaNet' if L.family == I.GDN else 'Mamba-2 SSD'} layer, "
+            f"{w.n_req} requests, {T} online tokens, {L.h_v} heads"
+            f"{f' ({L.h_qk} q/k)' if L.h_qk != L.h_v and L.family == I.GDN else ''}, dk={L.dk}, dv={L.dv}, "
+            f"chunk {L.chunk}, {w.n_blk} cached blocks ({w.cached.n_tok} tokens), bf16 inputs, fp32 state")
+
+
 # ---------------------------------------------------------------- main
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=50, help="timed steps (cold and warm each); medians reported")
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", type=int, default=3,
                     help="workload index (default 3: Gated DeltaNet, 32K context, 4 requests)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of CPU-oracle work")
     ap.add_argument("--no-decode", action="store_true",
                     help="skip the timings outside the step (decode, gather, staging, probe)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the other workloads (8K Gated DeltaNet, 8K Mamba-2, ragged 16K)")
+    ap.add_argument("--no-peaks", action="store_true", help="skip the measured-peak probes")
     ap.add_argument("--copy-probe", action="store_true",
                     help="after timing, run a plain 512 MiB device copy (counter calibration)")
     args = ap.parse_args()
@@ -393,6 +580,7 @@ def main():
     from paper_2608_11231_amd import inputs as I
 
     torch.cuda.set_device(0)
+    timer = Timer()
     tic = time.perf_counter()
     w = I.config(args.config, workers=16)
     log(f"[bench] workload {w.name}: {w.online.n_tok} online tokens, {w.cached.n_tok} cached tokens in "
@@ -401,57 +589,57 @@ def main():
     G.block_summary(B=True, M=False)        # the cache content: per-block states
     torch.cuda.synchronize()
     log("[bench] inputs resident in HBM; block states built")
-
-    ops = [("init_single", G.init_single),
-           ("fold", G.fold_transitions),
-           ("compose", G.init_compose),
-           ("scan", lambda: G.scan(G.S_exact))]
-
-    def step(events=None):
-        for i, (_, f) in enumerate(ops):
-            if events is not None:
-                events[i][0].record()
-            f()
-            if events is not None:
-                events[i][1].record()
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    ev = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)] for _ in ops]
-          for _ in range(args.steps)]
-    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_start.record()
-    for k in range(args.steps):
-        step(ev[k])
-    t_end.record()
-    torch.cuda.synchronize()
-    ms_step = t_start.elapsed_time(t_end) / args.steps
-    per_op = {name: float(np.mean([ev[k][i][0].elapsed_time(ev[k][i][1]) for k in range(args.steps)]))
-              for i, (name, _) in enumerate(ops)}
-    log("[bench] timed: " + ", ".join(f"{k} {v * 1e3:.1f} us" for k, v in per_op.items()))
+    m = measure(w, G, args.steps, args.warmup, timer)
+    log("[bench] cold medians: " + ", ".join(f"{k} {v['median_us']:.1f} us" for k, v in m["ops_cold"].items())
+        + f"; step {m['step_cold']['median_us']:.1f} us (warm {m['step_warm']['median_us']:.1f} us)")
 
     # LinearKV's path as one launch: the scan starting from the cached pool row
     from paper_2608_11231_amd import lkv
     fused = lambda: lkv.chunk_scan_from_pool(G.layer, G.online.struct, w.scale, G.B_pool, w.n_blk, G.last_blk,
                                              G.out, G.S_final)
-    for _ in range(3):
-        fused()
-    f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    f0.record()
-    for _ in range(args.steps):
-        fused()
-    f1.record()
-    torch.cuda.synchronize()
-    fused_us = f0.elapsed_time(f1) * 1e3 / args.steps
+    timer.run([("fused", fused)], 3, cold=False)
+    _, f_op = timer.run([("fused", fused)], args.steps, cold=True)
+    fused_us = stats(f_op["fused"])["median_us"]
     log(f"[bench] LinearKV path in one launch (scan from the pool row): {fused_us:.1f} us")
 
     decode = None if args.no_decode else decode_bench(w, G.S_final, args.steps)
     gather = None if args.no_decode else gather_bench(w, G, args.steps)
     staging = None if (args.no_decode or w.layer.family != I.GDN) else staging_bench(w, G, args.steps)
-    diag = None if args.no_decode else diag_bench(w, G, args.steps)
+    diag = None
+    if not args.no_decode:
+        diag = dict(default_gates=diag_bench(w, G, args.steps))
+        wm = I.config(args.config, mild=True, workers=16)
+        Gm = gpu_io.GpuWorkload(wm)
+        Gm.block_summary(B=True, M=False)
+        diag["mild_gates"] = diag_bench(wm, Gm, args.steps)
+        del Gm
+
+    others = {}
+    if not args.no_configs:
+        for idx in (1, 2, 4):
+            if idx == args.config:
+                continue
+            wo = I.config(idx, workers=16)
+            Go = gpu_io.GpuWorkload(wo)
+            Go.block_summary(B=True, M=False)
+            mo = measure(wo, Go, args.steps, args.warmup, timer)
+            mo["workload"] = workload_desc(wo)
+            others[wo.name] = mo
+            log(f"[bench] {wo.name} cold medians: " + ", ".join(
+                f"{k} {v['median_us']:.1f} us" for k, v in mo["ops_cold"].items())
+                + f"; step {mo['step_cold']['median_us']:.1f} us")
+            del Go
+
+    # measured denominators last, so that their heat does not slow the timings above
+    peaks = None
+    if not args.no_peaks:
+        peaks = measured_peaks()
+        log(f"[bench] measured peaks: HBM {peaks['hbm_GBs']:.0f} GB/s, bf16 matmul {peaks['bf16_TFLOPs']:.0f} "
+            f"TFLOP/s")
+        for r in [*m["roofline_by_kernel"].values(),
+                  *(x for o in others.values() for x in o["roofline_by_kernel"].values())]:
+            meas = peaks["hbm_GBs"] if r["bound"] == "hbm" else peaks["bf16_TFLOPs"]
+            r["frac_of_measured_peak"] = round(r["achieved"] / meas, 4)
 
     if args.copy_probe:
         src = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
@@ -461,66 +649,48 @@ def main():
         torch.cuda.synchronize()
 
     T = w.online.n_tok
-    work = work_model(w)
-    roofs = {name: roofline(name, work[name], per_op[name]) for name in per_op}
-    # measured HBM traffic per launch, from the committed rocprofv3 counter summary of
-    # this workload -- only when it was taken on the current kernel sources
-    from paper_2608_11231_amd import rocprof_summary
-    table = rocprof_summary.read_traffic(os.path.join(ROOT, "profiles", f"{w.name}_hbm_traffic.txt"))
-    if table:
-        fam = w.layer.family
-        def chunk_mode(n):
-            # lkv::chunk_kernel<FAM,DK,CH,F32IO,NB,SUMMARY,RT>: family and summary flag
-            if not n.startswith("lkv::chunk_kernel<"):
-                return None
-            args = n[len("lkv::chunk_kernel<"):].rstrip(">").split(",")
-            return (int(args[0]), args[5] == "true") if len(args) >= 6 else None
-
-        pick = {"scan": lambda n: chunk_mode(n) == (fam, False),
-                "fold": lambda n: chunk_mode(n) == (fam, True),
-                # the step composes from and copies out of fp32 pools (the <..., false> variants)
-                "compose": lambda n: "compose" in n and n.rstrip(">").endswith("false"),
-                "init_single": lambda n: "init_single" in n and n.rstrip(">").endswith("false")}
-        for op, pred in pick.items():
-            cand = [v for (n, grid), v in table.items() if pred(n)]
-            if len(cand) == 1:
-                roofs[op]["traffic"] = round(cand[0])
-    dominant = max(per_op, key=per_op.get)
     L = w.layer
+    roofs = m["roofline_by_kernel"]
     result = {
         "metric": "online linear-layer prefill tokens/s at 8K/32K; K-way composition latency (us)",
-        "value": round(T / (ms_step * 1e-3), 1),
+        "value": m["tokens_per_s"],
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 4),
+        "ms_per_step": round(m["step_cold"]["median_us"] * 1e-3, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
         "config": {
-            "workload": (f"{w.name}: {'Gated DeltaNet' if L.family == I.GDN else 'Mamba-2 SSD'} layer, "
-                         f"{w.n_req} requests x {T // max(w.n_req, 1)} online tokens, {L.h_v} heads, "
-                         f"dk={L.dk}, dv={L.dv}, chunk {L.chunk}, {w.n_blk} cached blocks "
-                         f"({w.cached.n_tok} tokens), bf16 inputs, fp32 state"),
+            "workload": workload_desc(w),
             "online_tokens": T,
             "cached_tokens": w.cached.n_tok,
             "cached_blocks": w.n_blk,
             "requests": w.n_req,
             "parallelism": "single GPU",
         },
-        "composition_latency_us": round(per_op["compose"] * 1e3, 2),
-        "fold_plus_compose_latency_us": round((per_op["fold"] + per_op["compose"]) * 1e3, 2),
-        "single_init_latency_us": round(per_op["init_single"] * 1e3, 2),
-        "scan_us": round(per_op["scan"] * 1e3, 2),
-        "lb_tokens_per_s": round(T / ((per_op["init_single"] + per_op["scan"]) * 1e-3), 1),
+        "timing": ("cold: each timed step preceded by an untimed 512 MiB buffer write (Infinity Cache "
+                   "evicted); value and per-kernel figures are medians over the cold steps; warm "
+                   "(back-to-back) figures alongside"),
+        "composition_latency_us": m["composition_latency_us"],
+        "fold_plus_compose_latency_us": m["fold_plus_compose_latency_us"],
+        "single_init_latency_us": m["single_init_latency_us"],
+        "scan_us": m["scan_us"],
+        "lb_tokens_per_s": m["lb_tokens_per_s"],
         "lb_fused_us": round(fused_us, 2),
         "lb_fused_tokens_per_s": round(T / (fused_us * 1e-6), 1),
-        "ex_tokens_per_s": round(T / ((per_op["fold"] + per_op["compose"] + per_op["scan"]) * 1e-3), 1),
-        "roofline": roofs[dominant],
+        "ex_tokens_per_s": m["ex_tokens_per_s"],
+        "step_cold": m["step_cold"],
+        "step_warm": m["step_warm"],
+        "ops_cold": m["ops_cold"],
+        "ops_warm": m["ops_warm"],
+        "measured_peaks": peaks,
+        "roofline": roofs[m["dominant"]],
         "roofline_by_kernel": roofs,
+        "other_workloads": others,
         "decode_step": decode,
         "gather_selected": gather,
         "bf16_pool_staging": staging,
