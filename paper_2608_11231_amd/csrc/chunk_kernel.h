@@ -312,6 +312,7 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
         // ---- the state: RT row tiles per wave, tile rt covering rows row_of(rt);
         // acc layout: S[rt][nt] holds S[row][16nt + 4g + r]
         auto row_of = [&](int rt) { return row0 + 16 * (RT * w + rt) + c16; };
+        const bf16x8 negI = neg_eye(g, c16);  // hi / lo splits on the matrix core
         f32x4 S[RT][NTK];
         // initial state row: segment s's own (S_init) or, with src, a pool row
         // (LinearKV's single cached state read straight from the cache pool)
@@ -352,7 +353,10 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
             for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
                 for (int nt = 0; nt < NTK; ++nt) {
-                    const Split4 sp = split4(S[rt][nt]);
+                    // 64-token chunks: S comes from a 32-wide MFMA chain, which the
+                    // 32-wide split product may follow; 16-token chunks update S
+                    // 16-wide, and one chain never mixes the two shapes
+                    const Split4 sp = NTC == 4 ? split4_mm(S[rt][nt], negI) : split4(S[rt][nt]);
                     Sh[rt][nt] = sp.hi;
                     Sl[rt][nt] = sp.lo;
                 }
@@ -507,14 +511,14 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                     }
                     auto split_u = [&](int rt, int mt, f32x4 v) {
                         U[rt][mt] = v;
-                        const Split4 us = split4(v);
+                        const Split4 us = split4_mm(v, negI);
                         Uh[rt][mt] = us.hi;
                         Ul[rt][mt] = us.lo;
                     };
                     if constexpr (NTC == 1) {
 #pragma unroll
                         for (int rt = 0; rt < RT; ++rt) {
-                            const Split4 xs = split4(X[rt][0]);
+                            const Split4 xs = split4_mm(X[rt][0], negI);
                             const f32x4 u0 = mma16(Nh[0], xs.hi, zero4());
                             f32x4 u1 = mma16(Nh[0], xs.lo, zero4());
                             u1 = mma16(Nl[0], xs.hi, u1);
@@ -537,7 +541,7 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                         // stage 1: U_0 = N_0 X_0, U_1 = T_10 X_0 + N_1 X_1
 #pragma unroll
                         for (int rt = 0; rt < RT; ++rt) {
-                            const Split4 x0 = split4(X[rt][0]), x1 = split4(X[rt][1]);
+                            const Split4 x0 = split4_mm(X[rt][0], negI), x1 = split4_mm(X[rt][1], negI);
                             const f32x4 u0h = mma16(Nh[0], x0.hi, zero4());
                             const f32x4 u1h = mma32(t10h, Nh[1], x0.hi, x1.hi, zero4());
                             f32x4 u0l = mma16(Nh[0], x0.lo, zero4());
@@ -557,8 +561,8 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                             f32x4 r3l = mma32(Lh[2], Lh[3], Ul[rt][0], Ul[rt][1], zero4());
                             r2l = mma32(Ll[0], Ll[1], Uh[rt][0], Uh[rt][1], r2l);
                             r3l = mma32(Ll[2], Ll[3], Uh[rt][0], Uh[rt][1], r3l);
-                            x2[rt] = split4(r2h + r2l);
-                            x3[rt] = split4(r3h + r3l);
+                            x2[rt] = split4_mm(r2h + r2l, negI);
+                            x3[rt] = split4_mm(r3h + r3l, negI);
                         }
                         // stage 3: U_2 = N_2 R_2, U_3 = T_32 R_2 + N_3 R_3
 #pragma unroll
@@ -637,7 +641,7 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                     const f32x4 wt = lds4f(G + 3 * CH + 16 * mt + 4 * g);
 #pragma unroll
                     for (int rt = 0; rt < RT; ++rt) {
-                        const Split4 sp = split4(wt * U[rt][mt]);
+                        const Split4 sp = split4_mm(wt * U[rt][mt], negI);
                         Wh[rt][mt] = sp.hi;
                         Wl[rt][mt] = sp.lo;
                     }

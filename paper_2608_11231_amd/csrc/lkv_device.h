@@ -87,6 +87,28 @@ __device__ __forceinline__ Split4 split4(f32x4 x) {
     return s;
 }
 
+// The same split with x - hi formed on the matrix core: one 16x16x32 product
+// of the negated identity (A) with the acc tile's own hi parts (B, upper 16-slice
+// zero), accumulated onto x.  Every product but one per output is an exact zero
+// and x - hi is representable, so the result is bit-identical to split4 while
+// the unpack and subtract of every value (two VALU instructions) become a
+// quarter of an MFMA.  neg_eye: lane (g, c) holds -1 at element j when 4g + j
+// == c (the contraction bijection above, first 16-slice), zero elsewhere.
+__device__ __forceinline__ bf16x8 neg_eye(int g, int c) {
+    bf16x8 e;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) e[j] = (j < 4 && 4 * g + j == c) ? (bf16)-1.f : (bf16)0.f;
+    return e;
+}
+__device__ __forceinline__ Split4 split4_mm(f32x4 x, bf16x8 negI) {
+    Split4 s;
+    s.hi = to_bf16(x);
+    const bf16x8 b = __builtin_shufflevector(s.hi, bf16x4{(bf16)0.f, (bf16)0.f, (bf16)0.f, (bf16)0.f},
+                                             0, 1, 2, 3, 4, 5, 6, 7);
+    s.lo = to_bf16(__builtin_amdgcn_mfma_f32_16x16x32_bf16(negI, b, x, 0, 0, 0));
+    return s;
+}
+
 // LDS loads of 4 / 8 consecutive elements (8 / 16 / 16 bytes)
 __device__ __forceinline__ bf16x4 lds4(const bf16* p) { return *reinterpret_cast<const bf16x4*>(p); }
 __device__ __forceinline__ bf16x8 lds8(const bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
