@@ -25,6 +25,5 @@ hipError_t launch_compose_ssd(int32_t n_req, int32_t n_blk, int32_t H, int64_t p
 hipError_t launch_compose_gdn(int dk, const ComposeArgs& a, hipStream_t st);
 hipError_t launch_ssd_lambda(const int32_t* cu, int32_t n_seq, int64_t n_tok, int32_t H, const float* dt,
                              const float* A, float* Lam, hipStream_t st);
-size_t compose_gdn_lds_bytes(int dk);
 
 }  // namespace lkv

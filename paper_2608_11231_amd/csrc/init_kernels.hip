@@ -174,27 +174,42 @@ hipError_t launch_compose_ssd(int32_t n_req, int32_t n_blk, int32_t H, int64_t p
 // products Mh*Sh + Mh*Sl + Ml*Sh keep the fp32 chain at ~1e-5 relative) and
 // reads the M^T fragments with transposed LDS loads.
 //
-// The loop is software-pipelined: while block j is multiplied, the next
-// block's M (all of it, spread over the workgroup) and this lane's rows of its
-// B are already in flight from HBM into registers, so every step overlaps one
-// full block of loads with the products of the previous one.
+// Software pipeline over the request's blocks: step j multiplies by M_j
+// (staged in LDS one step earlier), then stages M_{j+1}, loaded one step
+// earlier, and issues the loads of M_{j+2}; B_{j+1}'s rows are requested as
+// soon as B_j has seeded the accumulators.  The two barriers of a step order
+// LDS only (s_barrier after an LDS wait), so the global loads stay in flight
+// across them, and nothing in the loop waits for every load in flight (see
+// the block ids below).  Rows of a staged plane are DK + 16 elements apart,
+// which keeps the transposed fragment reads free of bank conflicts; the LDS
+// footprint (74 KB at dk = 128) lets two workgroups share a CU.
 template <int DK>
 struct ComposeLds {
-    static constexpr int SM = DK + 8;
-    static __host__ __device__ constexpr size_t bytes() { return size_t(2) * DK * SM * 2; }
+    static constexpr int SM = DK >= 32 ? DK + 16 : DK + 8;
+    static constexpr size_t PLANE = size_t(DK) * SM;  // elements
+    static __host__ __device__ constexpr size_t bytes() { return 2 * PLANE * 2; }
 };
 
 template <int DK, int NW, bool BF>
 __global__ __launch_bounds__(64 * NW) void compose_gdn_kernel(ComposeArgs p) {
-    constexpr int NTK = DK / 16, SM = ComposeLds<DK>::SM;
+    using Ly = ComposeLds<DK>;
+    constexpr int NTK = DK / 16, SM = Ly::SM;
     constexpr int NTH = 64 * NW;
     constexpr int NV = DK * DK / 4;              // float4 vectors of one M
     constexpr int PER = (NV + NTH - 1) / NTH;    // of them per thread
+    // the matrix-core split needs every lane of the wave; it is used where each
+    // thread stages whole vectors and the state chain is 32 wide.  The staging
+    // of M uses it with four waves only: a smaller workgroup stages M with as
+    // many split products per wave as it has state products, and that wave's
+    // matrix-core time becomes the step's
+    constexpr bool MM_SPLIT = NV % NTH == 0 && NTK % 2 == 0;
+    constexpr bool MM_SPLIT_M = MM_SPLIT && NW == 4;
     extern __shared__ __align__(16) char smem[];
     bf16* sMh = reinterpret_cast<bf16*>(smem);
-    bf16* sMl = sMh + DK * SM;
+    bf16* sMl = sMh + Ly::PLANE;
     const int tid = threadIdx.x;
     const int w = tid >> 6, lane = tid & 63, g = lane >> 4, c16 = lane & 15;
+    const bf16x8 negI = neg_eye(g, c16);
     // units: the row tiles of one (request, head) adjacent, then the request
     // index fastest, so each XCD's range holds a few heads of every request
     // (ragged block counts load the XCDs evenly)
@@ -214,96 +229,125 @@ __global__ __launch_bounds__(64 * NW) void compose_gdn_kernel(ComposeArgs p) {
         return (((int64_t)id * p.h_v + h) * p.dv + my_row) * DK + 4 * g;
     };
     f32x4 mreg[PER], breg[NTK];
-    auto prefetch = [&](int32_t id) {
+    auto load_m = [&](int32_t id) {
+        // plain loads: the head's other row tiles read the same M through the XCD's L2
         const f32x4* Mj = reinterpret_cast<const f32x4*>(p.M_pool + ((int64_t)id * p.h_v + h) * DK * DK);
 #pragma unroll
         for (int i = 0; i < PER; ++i) {
             const int idx = tid + i * NTH;
-            if (NV % NTH == 0 || idx < NV) mreg[i] = Mj[idx];  // shared by the head's row tiles (L2)
+            if (NV % NTH == 0 || idx < NV) mreg[i] = Mj[idx];
         }
+    };
+    auto load_b = [&](int32_t id) {
         const int64_t Bj = b_rows(id);
 #pragma unroll
         for (int nt = 0; nt < NTK; ++nt) breg[nt] = pool4<BF>(p.B_pool, Bj + 16 * nt);
     };
-
-    f32x4 S[NTK];
-#pragma unroll
-    for (int nt = 0; nt < NTK; ++nt) S[nt] = zero4();
-    bool bad = false;
-    if (b0 < b1) {
-        const int32_t id0 = p.blk_ids[b0];
-        if (!valid(id0)) {
-            bad = true;
-        } else {
-            const int64_t B0 = b_rows(id0);
-#pragma unroll
-            for (int nt = 0; nt < NTK; ++nt) S[nt] = pool4<BF>(p.B_pool, B0 + 16 * nt);
-        }
-    }
-    int32_t id_next = (!bad && b0 + 1 < b1) ? p.blk_ids[b0 + 1] : 0;
-    if (!bad && b0 + 1 < b1 && valid(id_next)) prefetch(id_next);
-    for (int32_t j = b0 + 1; j < b1 && !bad; ++j) {
-        if (!valid(id_next)) {  // uniform over the workgroup: every wave leaves together
-            bad = true;
-            break;
-        }
-        // stage M_j (prefetched) row-major, split into bf16 hi / lo planes
-        __syncthreads();
+    // M (in mreg) -> bf16 hi / lo planes in LDS, row-major
+    auto stage_m = [&]() {
 #pragma unroll
         for (int i = 0; i < PER; ++i) {
             const int idx = tid + i * NTH;
             if (NV % NTH != 0 && idx >= NV) continue;
             const int ii = idx / (DK / 4), jj = (idx % (DK / 4)) * 4;
-            const Split4 sp = split4(mreg[i]);
+            const Split4 sp = MM_SPLIT_M ? split4_mm(mreg[i], negI) : split4(mreg[i]);
             *reinterpret_cast<bf16x4*>(sMh + ii * SM + jj) = sp.hi;
             *reinterpret_cast<bf16x4*>(sMl + ii * SM + jj) = sp.lo;
         }
+    };
+
+    // The request's block ids are read through the scalar cache (a constant
+    // address-space view of the read-only id array): their waits count on the
+    // scalar/LDS counter, so reading an id never waits for the prefetched M and
+    // B loads in flight on the vector-memory counter.
+    typedef __attribute__((address_space(4))) const int32_t const_i32;
+    const const_i32* ids_c = (const const_i32*)p.blk_ids;
+    auto id_at = [&](int32_t j) { return ids_c[j]; };
+    f32x4 S[NTK];
+#pragma unroll
+    for (int nt = 0; nt < NTK; ++nt) S[nt] = zero4();
+    // block ids are the same for every wave of the workgroup, so every branch
+    // on them below is uniform; bad_at is the first position with an invalid id
+    int32_t bad_at = b1;
+    auto id_checked = [&](int32_t j) {
+        const int32_t id = id_at(j);
+        if (!valid(id) && j < bad_at) bad_at = j;
+        return id;
+    };
+    // Step j (b0 <= j < b1) starts with B_j in breg, M_{j+1} in mreg and, past
+    // the first step, M_j staged in LDS; it seeds the accumulators
+    // with B_j, requests B_{j+1}, adds M_j^T S^T (not on the first step, which
+    // only takes S = B_{b0}), stages M_{j+1} and requests M_{j+2}.  Every step
+    // has the same shape, so the state never comes straight from a load and
+    // the prefetch registers carry the same in-flight loads at the top of
+    // every step.  Loads past the request's end re-read the block loaded
+    // just before (a cache hit; unconditional loads keep the prefetch
+    // registers single-valued).
+    int32_t id0 = 0, id1 = 0, id2 = 0;  // ids at positions j, j + 1, j + 2
+    if (b0 < b1) id0 = id_checked(b0);
+    if (b0 + 1 < b1) id1 = id_checked(b0 + 1);
+    if (b0 < bad_at) {
+        load_b(id0);
+        load_m(b0 + 1 < bad_at ? id1 : id0);
+    }
+    for (int32_t j = b0; j < b1 && j < bad_at; ++j) {
+        if (j + 2 < b1) id2 = id_checked(j + 2);
+        lds_barrier();  // M_j staged by every wave
         f32x4 acc[NTK];
 #pragma unroll
         for (int nt = 0; nt < NTK; ++nt) acc[nt] = breg[nt];
-        __syncthreads();
-        // the next block's loads go out before this block's products
-        id_next = j + 1 < b1 ? p.blk_ids[j + 1] : 0;
-        if (j + 1 < b1 && valid(id_next)) prefetch(id_next);
-        bf16x4 Sh[NTK], Sl[NTK];
+        load_b(j + 1 < bad_at ? id1 : id0);
+        // B_{j+1} stays ahead of M_{j+2} in issue order: the memory counter is
+        // in order, so waiting for one waits for everything issued before it
+        __builtin_amdgcn_sched_barrier(0);
+        if (j > b0) {
+            bf16x4 Sh[NTK], Sl[NTK];
 #pragma unroll
-        for (int nt = 0; nt < NTK; ++nt) {
-            const Split4 sp = split4(S[nt]);
-            Sh[nt] = sp.hi;
-            Sl[nt] = sp.lo;
-        }
-        // S_new^T tile nt (rows 16nt..16nt+15) = M^T S^T + B^T: A fragments of M^T
-        // come straight from the row-major planes through transposed LDS reads;
-        // the dk tiles are interleaved so NTK accumulation chains are in flight
-        if constexpr (NTK == 1) {
-            const bf16x4 a0 = lds4_tr(sMh, SM, 0, 0, g, c16);
-            const bf16x4 c0 = lds4_tr(sMl, SM, 0, 0, g, c16);
-            acc[0] = mma16(a0, Sh[0], acc[0]);
-            acc[0] = mma16(a0, Sl[0], acc[0]);
-            acc[0] = mma16(c0, Sh[0], acc[0]);
-        } else {
+            for (int nt = 0; nt < NTK; ++nt) {
+                const Split4 sp = MM_SPLIT ? split4_mm(S[nt], negI) : split4(S[nt]);
+                Sh[nt] = sp.hi;
+                Sl[nt] = sp.lo;
+            }
+            // S_new^T tile nt (rows 16nt..16nt+15) = M^T S^T + B^T: A fragments of
+            // M^T come straight from the row-major planes through transposed LDS
+            // reads; the dk tiles are interleaved so NTK accumulation chains are in
+            // flight
+            if constexpr (NTK == 1) {
+                const bf16x4 a0 = lds4_tr(sMh, SM, 0, 0, g, c16);
+                const bf16x4 c0 = lds4_tr(sMl, SM, 0, 0, g, c16);
+                acc[0] = mma16(a0, Sh[0], acc[0]);
+                acc[0] = mma16(a0, Sl[0], acc[0]);
+                acc[0] = mma16(c0, Sh[0], acc[0]);
+            } else {
 #pragma unroll
-            for (int kg = 0; kg < NTK; kg += 2) {
-                bf16x4 a0[NTK], a1[NTK], c0[NTK], c1[NTK];
+                for (int kg = 0; kg < NTK; kg += 2) {
+                    bf16x4 a0[NTK], a1[NTK], c0[NTK], c1[NTK];
 #pragma unroll
-                for (int nt = 0; nt < NTK; ++nt) {
-                    a0[nt] = lds4_tr(sMh, SM, 16 * kg, 16 * nt, g, c16);
-                    a1[nt] = lds4_tr(sMh, SM, 16 * kg + 16, 16 * nt, g, c16);
-                    c0[nt] = lds4_tr(sMl, SM, 16 * kg, 16 * nt, g, c16);
-                    c1[nt] = lds4_tr(sMl, SM, 16 * kg + 16, 16 * nt, g, c16);
-                }
+                    for (int nt = 0; nt < NTK; ++nt) {
+                        a0[nt] = lds4_tr(sMh, SM, 16 * kg, 16 * nt, g, c16);
+                        a1[nt] = lds4_tr(sMh, SM, 16 * kg + 16, 16 * nt, g, c16);
+                        c0[nt] = lds4_tr(sMl, SM, 16 * kg, 16 * nt, g, c16);
+                        c1[nt] = lds4_tr(sMl, SM, 16 * kg + 16, 16 * nt, g, c16);
+                    }
 #pragma unroll
-                for (int nt = 0; nt < NTK; ++nt) {
-                    acc[nt] = mma32(a0[nt], a1[nt], Sh[kg], Sh[kg + 1], acc[nt]);
-                    acc[nt] = mma32(a0[nt], a1[nt], Sl[kg], Sl[kg + 1], acc[nt]);
-                    acc[nt] = mma32(c0[nt], c1[nt], Sh[kg], Sh[kg + 1], acc[nt]);
+                    for (int nt = 0; nt < NTK; ++nt) {
+                        acc[nt] = mma32(a0[nt], a1[nt], Sh[kg], Sh[kg + 1], acc[nt]);
+                        acc[nt] = mma32(a0[nt], a1[nt], Sl[kg], Sl[kg + 1], acc[nt]);
+                        acc[nt] = mma32(c0[nt], c1[nt], Sh[kg], Sh[kg + 1], acc[nt]);
+                    }
                 }
             }
         }
+        // stage M_{j+1} (requested one step ago) and request M_{j+2}
+        lds_barrier();  // every wave is done reading M_j
+        stage_m();
+        load_m(j + 2 < bad_at ? id2 : id1);
 #pragma unroll
         for (int nt = 0; nt < NTK; ++nt) S[nt] = acc[nt];
+        id0 = id1;
+        id1 = id2;
     }
-    if (bad) {
+    if (bad_at < b1) {
         const float f = __builtin_nanf("");
 #pragma unroll
         for (int nt = 0; nt < NTK; ++nt) S[nt] = f32x4{f, f, f, f};
@@ -311,16 +355,6 @@ __global__ __launch_bounds__(64 * NW) void compose_gdn_kernel(ComposeArgs p) {
     float* dst = p.S + (((int64_t)r * p.h_v + h) * p.dv + my_row) * DK + 4 * g;
 #pragma unroll
     for (int nt = 0; nt < NTK; ++nt) *reinterpret_cast<f32x4*>(dst + 16 * nt) = S[nt];
-}
-
-size_t compose_gdn_lds_bytes(int dk) {
-    switch (dk) {
-        case 16: return ComposeLds<16>::bytes();
-        case 32: return ComposeLds<32>::bytes();
-        case 64: return ComposeLds<64>::bytes();
-        case 128: return ComposeLds<128>::bytes();
-    }
-    return 0;
 }
 
 template <int DK, int NW>

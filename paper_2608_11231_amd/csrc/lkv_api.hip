@@ -203,12 +203,13 @@ lkv_status init_compose(const lkv_layer* L, int32_t n_req, int32_t n_blk, const 
                                              blk_cu, n_ids, S_init, st));
     }
     const int64_t pairs = (int64_t)n_req * L->h_v;
+    // state-row waves per workgroup: four (64 rows) wherever dv allows.  Each
+    // step stages the whole M in LDS; four waves share that staging, and the
+    // step's latency -- not the number of workgroups -- sets the time (at 8K,
+    // 64 four-wave workgroups compose faster than 256 one-wave ones)
     int nw = env_int("LKV_COMPOSE_NW", 0);
-    if (nw != 1 && nw != 2 && nw != 4) {
-        nw = 4;
-        while (nw > 1 && (L->dv % (16 * nw) || pairs * (L->dv / (16 * nw)) < 240)) nw >>= 1;
-    }
-    if (L->dv % (16 * nw)) nw = 1;
+    if (nw != 1 && nw != 2 && nw != 4) nw = 4;
+    while (nw > 1 && L->dv % (16 * nw)) nw >>= 1;
     ComposeArgs a = {};
     a.B_pool = B_pool;
     a.bf16_pool = bf16_pool;
