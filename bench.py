@@ -511,10 +511,12 @@ def measure(w, G, steps: int, warmup: int, timer: Timer):
     """The step's four calls on workload ``w``: cold (the headline: Infinity Cache
     flushed before every step, medians) and warm (back to back).  Returns the
     per-op and per-step figures, the rooflines and the two paths' rates."""
+    from paper_2608_11231_amd.gpu_io import sp_pieces
+    pieces = sp_pieces(w)  # sequence-parallel scan where the (request, head) chains underfill the GPU
     ops = [("init_single", G.init_single),
            ("fold", G.fold_transitions),
            ("compose", G.init_compose),
-           ("scan", lambda: G.scan(G.S_exact))]
+           ("scan", lambda: G.scan(G.S_exact, pieces=pieces))]
     timer.run(ops, warmup, cold=False)
     cold_step, cold_op = timer.run(ops, steps, cold=True)
     warm_step, warm_op = timer.run(ops, steps, cold=False)
@@ -539,7 +541,8 @@ def measure(w, G, steps: int, warmup: int, timer: Timer):
         composition_latency_us=round(med["compose"] * 1e3, 2),
         fold_plus_compose_latency_us=round((med["fold"] + med["compose"]) * 1e3, 2),
         single_init_latency_us=round(med["init_single"] * 1e3, 2),
-        scan_us=round(med["scan"] * 1e3, 2))
+        scan_us=round(med["scan"] * 1e3, 2),
+        scan_pieces=pieces)
 
 
 def workload_desc(w):

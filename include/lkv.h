@@ -44,7 +44,7 @@
 extern "C" {
 #endif
 
-#define LKV_ABI_VERSION 7
+#define LKV_ABI_VERSION 8
 
 typedef enum {
     LKV_OK = 0,
@@ -200,6 +200,39 @@ lkv_status lkv_ssd_chunk_scan(const lkv_layer* layer, const lkv_tokens* online,
 lkv_status lkv_chunk_scan_from_pool(const lkv_layer* layer, const lkv_tokens* online, float scale,
                                     const void* B_pool, int32_t pool_dtype, int32_t n_blk,
                                     const int32_t* src_blk, void* out, float* S_final, void* stream);
+
+/* Sequence-parallel chunk scan.  The results of lkv_gdn_chunk_scan /
+ * lkv_ssd_chunk_scan (by layer->family; `scale` is ignored for Mamba-2),
+ * computed with the sequence dimension split: each request's online stream
+ * is cut into `pieces` consecutive pieces of whole chunks (the last takes the
+ * remainder; trailing pieces may be empty), and the recurrence is Eq. 5
+ * applied piece after piece.  Every piece's pair (its end state from zero and
+ * its transition -- the dense M of Gated DeltaNet, the log-decay of Mamba-2)
+ * is computed at once, as by lkv_block_summary; composing the request's
+ * initial state with the pairs of pieces 0..p-1 (Eq. 6 from a non-empty
+ * prefix, as lkv_init_compose) gives piece p's start state and, after the last
+ * piece, the final state; then every piece is scanned from its start state,
+ * all at once, for the outputs.  The chain of dependent chunks per request is
+ * about pieces times shorter, at the price of the pieces' transitions
+ * (Gated DeltaNet: about twice the state work of a scan without outputs;
+ * Mamba-2: a sum of dt) and the composition: it pays when few (request, head)
+ * chains leave the GPU idle, e.g. one 8K request.  Results agree with the
+ * serial scan within the fp32 state tolerance (they are not bit-identical:
+ * the rounding order differs).
+ *   pieces   1..64
+ *   ws       device workspace of at least lkv_chunk_scan_sp_workspace bytes,
+ *            256-byte aligned, caller-owned; its contents on entry do not
+ *            matter and are overwritten.  Calls that share a workspace race
+ *            unless ordered by a stream.
+ * Other arguments as in lkv_gdn_chunk_scan (S_init may be NULL: zero start;
+ * S_final may be NULL, but S_init must not alias S_final here).  Errors:
+ * LKV_E_NULL, LKV_E_SHAPE (also a workspace too small), LKV_E_DTYPE,
+ * LKV_E_ALIGN, LKV_E_UNSUPPORTED, LKV_E_HIP. */
+lkv_status lkv_chunk_scan_sp_workspace(const lkv_layer* layer, int32_t n_req, int32_t pieces,
+                                       size_t* bytes);
+lkv_status lkv_chunk_scan_sp(const lkv_layer* layer, const lkv_tokens* online, float scale,
+                             const float* S_init, void* out, float* S_final, int32_t pieces,
+                             void* ws, size_t ws_bytes, void* stream);
 
 /* Decode step: the step that follows the online prefill, which keeps only the
  * final state for it (Sec. 2).  One new token per request advances each

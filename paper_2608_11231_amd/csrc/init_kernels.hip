@@ -68,13 +68,15 @@ hipError_t launch_init_single(int32_t n_req, int32_t n_blk, int64_t per_req, con
 
 // ---------------------------------------------------------------- Mamba-2 composition
 // S <- B_{b_1}; S <- exp(Lambda_{b_j}) S + B_{b_j}.  Elementwise over the state.
+// With S_steps, the state after each block but the request's last is also
+// stored (request r's position j at row j - r).
 template <bool BF>
 __global__ __launch_bounds__(256) void compose_ssd_kernel(int32_t n_req, int32_t n_blk, int32_t H,
                                                           int64_t per_head4, const void* __restrict__ B_pool,
                                                           const float* __restrict__ Lam,
                                                           const int32_t* __restrict__ ids,
                                                           const int32_t* __restrict__ blk_cu, int32_t n_ids,
-                                                          f32x4* __restrict__ S) {
+                                                          f32x4* __restrict__ S, f32x4* __restrict__ S_steps) {
     const int64_t total = (int64_t)n_req * H * per_head4;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
@@ -95,6 +97,7 @@ __global__ __launch_bounds__(256) void compose_ssd_kernel(int32_t n_req, int32_t
                 const float a = __expf(Lam[(int64_t)id * H + h]);
                 acc = a * acc + b;
             }
+            if (S_steps && j + 1 < b1) S_steps[((int64_t)(j - r) * H + h) * per_head4 + e] = acc;
         }
         if (bad) {
             const float f = __builtin_nanf("");
@@ -154,14 +157,14 @@ hipError_t launch_ssd_lambda(const int32_t* cu, int32_t n_seq, int64_t n_tok, in
 
 hipError_t launch_compose_ssd(int32_t n_req, int32_t n_blk, int32_t H, int64_t per_head, const void* B_pool,
                               bool bf16_pool, const float* Lam, const int32_t* ids, const int32_t* blk_cu,
-                              int32_t n_ids, float* S, hipStream_t st) {
+                              int32_t n_ids, float* S, float* S_steps, hipStream_t st) {
     const int64_t total = (int64_t)n_req * H * (per_head / 4);
     if (total == 0) return hipSuccess;
     int64_t blocks = (total + 255) / 256;
     if (blocks > 256 * 16) blocks = 256 * 16;
     auto kern = bf16_pool ? compose_ssd_kernel<true> : compose_ssd_kernel<false>;
     hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(256), 0, st, n_req, n_blk, H, per_head / 4, B_pool,
-                       Lam, ids, blk_cu, n_ids, reinterpret_cast<f32x4*>(S));
+                       Lam, ids, blk_cu, n_ids, reinterpret_cast<f32x4*>(S), reinterpret_cast<f32x4*>(S_steps));
     return hipGetLastError();
 }
 
@@ -182,7 +185,9 @@ hipError_t launch_compose_ssd(int32_t n_req, int32_t n_blk, int32_t H, int64_t p
 // across them, and nothing in the loop waits for every load in flight (see
 // the block ids below).  Rows of a staged plane are DK + 16 elements apart,
 // which keeps the transposed fragment reads free of bank conflicts; the LDS
-// footprint (74 KB at dk = 128) lets two workgroups share a CU.
+// footprint (74 KB at dk = 128) lets two workgroups share a CU.  With S_steps,
+// the state after each block but the request's last is also stored (request
+// r's position j at row j - r).
 template <int DK>
 struct ComposeLds {
     static constexpr int SM = DK >= 32 ? DK + 16 : DK + 8;
@@ -344,6 +349,12 @@ __global__ __launch_bounds__(64 * NW) void compose_gdn_kernel(ComposeArgs p) {
         load_m(j + 2 < bad_at ? id2 : id1);
 #pragma unroll
         for (int nt = 0; nt < NTK; ++nt) S[nt] = acc[nt];
+        if (p.S_steps && j + 1 < b1) {
+            // the state after this block (position j), a start state for a later step
+            float* dst = p.S_steps + ((((int64_t)j - r) * p.h_v + h) * p.dv + my_row) * DK + 4 * g;
+#pragma unroll
+            for (int nt = 0; nt < NTK; ++nt) *reinterpret_cast<f32x4*>(dst + 16 * nt) = acc[nt];
+        }
         id0 = id1;
         id1 = id2;
     }

@@ -8,6 +8,7 @@
 #include "diag_kernels.h"
 #include "gather_kernels.h"
 #include "pool_kernels.h"
+#include "sp_kernels.h"
 #include "init_kernels.h"
 #include "lkv.h"
 #include "chunk_kernel.h"
@@ -187,7 +188,7 @@ lkv_status init_single(const lkv_layer* L, int32_t n_req, int32_t n_blk, const v
 
 lkv_status init_compose(const lkv_layer* L, int32_t n_req, int32_t n_blk, const void* B_pool, bool bf16_pool,
                         const float* M_pool, const int32_t* blk_ids, const int32_t* blk_cu, int32_t n_ids,
-                        float* S_init, void* stream) {
+                        float* S_init, void* stream, float* S_steps = nullptr) {
     lkv_status s = check_layer(L);
     if (s != LKV_OK) return s;
     if (n_req < 0 || n_blk < 0 || n_ids < 0) return LKV_E_SHAPE;
@@ -200,7 +201,7 @@ lkv_status init_compose(const lkv_layer* L, int32_t n_req, int32_t n_blk, const 
     if (L->family == LKV_SSD) {
         const int64_t per_head = (int64_t)L->dv * L->dk;
         return hip_status(launch_compose_ssd(n_req, n_blk, L->h_v, per_head, B_pool, bf16_pool, M_pool, blk_ids,
-                                             blk_cu, n_ids, S_init, st));
+                                             blk_cu, n_ids, S_init, S_steps, st));
     }
     const int64_t pairs = (int64_t)n_req * L->h_v;
     // state-row waves per workgroup: four (64 rows) wherever dv allows.  Each
@@ -221,12 +222,90 @@ lkv_status init_compose(const lkv_layer* L, int32_t n_req, int32_t n_blk, const 
     a.h_v = L->h_v;
     a.dv = L->dv;
     a.S = S_init;
+    a.S_steps = S_steps;
     a.nw = nw;
     a.tiles = L->dv / (16 * nw);
     const int64_t units = pairs * a.tiles;
     if (units >= (INT64_C(1) << 31)) return LKV_E_SHAPE;
     a.n_units = (int32_t)units;
     return hip_status(launch_compose_gdn(L->dk, a, st));
+}
+
+// Workspace of the sequence-parallel scan, each region 256-byte aligned:
+// piece offsets, the composition's block ids and offsets, the block pools
+// (every piece's end state from zero and transition, then one row per
+// request holding its initial state), and every piece's start state.
+struct SpLayout {
+    size_t piece_cu, blk_ids, blk_cu, B, M, S_start, S_last, total;
+};
+
+SpLayout sp_layout(const lkv_layer* L, int64_t n_req, int64_t pieces) {
+    auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
+    const int64_t n_seg = n_req * pieces;
+    const size_t state = (size_t)L->h_v * L->dv * L->dk * 4;
+    const size_t trans = L->family == LKV_GDN ? (size_t)L->h_v * L->dk * L->dk * 4 : (size_t)L->h_v * 4;
+    SpLayout o{};
+    size_t at = 0;
+    o.piece_cu = at; at += up((size_t)(n_seg + 1) * 4);
+    o.blk_ids = at;  at += up((size_t)n_req * (pieces + 1) * 4);
+    o.blk_cu = at;   at += up((size_t)(n_req + 1) * 4);
+    o.B = at;        at += up((size_t)(n_seg + n_req) * state);
+    o.M = at;        at += up((size_t)(n_seg + n_req) * trans);
+    o.S_start = at;  at += up((size_t)n_seg * state);
+    o.S_last = at;   at += up((size_t)n_req * state);  // the final states when S_final is NULL
+    o.total = at;
+    return o;
+}
+
+lkv_status sp_check(const lkv_layer* L, int32_t n_req, int32_t pieces) {
+    lkv_status s = check_layer(L);
+    if (s != LKV_OK) return s;
+    if (n_req < 0 || pieces < 1 || pieces > 64) return LKV_E_SHAPE;
+    if ((int64_t)n_req * (pieces + 1) >= (INT64_C(1) << 31)) return LKV_E_SHAPE;
+    return LKV_OK;
+}
+
+lkv_status chunk_scan_sp(const lkv_layer* L, const lkv_tokens* T, float scale, const float* S_init, void* out,
+                         float* S_final, int32_t pieces, char* ws, size_t ws_bytes, void* stream) {
+    if (!T) return LKV_E_NULL;
+    lkv_status s = sp_check(L, T->n_seq, pieces);
+    if (s != LKV_OK) return s;
+    s = check_tokens(L, T, out != nullptr);
+    if (s != LKV_OK) return s;
+    if ((S_init && !aligned16(S_init)) || (S_final && !aligned16(S_final))) return LKV_E_ALIGN;
+    if (T->n_seq == 0 || (!out && !S_final)) return LKV_OK;
+    const SpLayout ly = sp_layout(L, T->n_seq, pieces);
+    if (!ws) return LKV_E_NULL;
+    if (((uintptr_t)ws & 255u) != 0) return LKV_E_ALIGN;
+    if (ws_bytes < ly.total) return LKV_E_SHAPE;
+    hipStream_t st = (hipStream_t)stream;
+    const int32_t n_req = T->n_seq, n_seg = n_req * pieces;
+    int32_t* piece_cu = reinterpret_cast<int32_t*>(ws + ly.piece_cu);
+    int32_t* blk_ids = reinterpret_cast<int32_t*>(ws + ly.blk_ids);
+    int32_t* blk_cu = reinterpret_cast<int32_t*>(ws + ly.blk_cu);
+    float* Bp = reinterpret_cast<float*>(ws + ly.B);
+    float* Mp = reinterpret_cast<float*>(ws + ly.M);
+    float* S_start = reinterpret_cast<float*>(ws + ly.S_start);
+    float* S_last = S_final ? S_final : reinterpret_cast<float*>(ws + ly.S_last);
+    const int64_t state = (int64_t)L->h_v * L->dv * L->dk;
+    lkv_status e = hip_status(launch_sp_setup(T->cu, n_req, pieces, L->chunk, T->n_tok, piece_cu, blk_ids, blk_cu,
+                                              S_init, Bp + (int64_t)n_seg * state, state, st));
+    if (e != LKV_OK) return e;
+    // every piece's (transition, state from zero): Eq. 5 per piece, one launch
+    lkv_tokens Tp = *T;
+    Tp.cu = piece_cu;
+    Tp.n_seq = n_seg;
+    Tp.q = nullptr;
+    e = lkv_block_summary(L, &Tp, Bp, Mp, stream);
+    if (e != LKV_OK) return e;
+    // the pieces' start states and the final state: each request's initial
+    // state composed with its pieces' pairs, the state after every piece kept
+    e = init_compose(L, n_req, n_seg + n_req, Bp, false, Mp, blk_ids, blk_cu, n_req * (pieces + 1), S_last, stream,
+                     S_start);
+    if (e != LKV_OK || !out) return e;
+    // the outputs: every piece scanned from its start state, all at once
+    Tp.q = T->q;
+    return chunk_scan(L, &Tp, L->family == LKV_GDN ? scale : 1.f, S_start, out, nullptr, stream);
 }
 
 }  // namespace
@@ -435,6 +514,19 @@ lkv_status lkv_chunk_scan_from_pool(const lkv_layer* L, const lkv_tokens* T, flo
     // with n_blk = 0 every id is -1 (zero state) or invalid (NaN): the pool is never read
     return chunk_scan(L, T, L->family == LKV_GDN ? scale : 1.f, reinterpret_cast<const float*>(B_pool), out,
                       S_final, stream, src_blk, n_blk, pool_dtype == LKV_BF16);
+}
+
+lkv_status lkv_chunk_scan_sp_workspace(const lkv_layer* L, int32_t n_req, int32_t pieces, size_t* bytes) {
+    if (!bytes) return LKV_E_NULL;
+    lkv_status s = sp_check(L, n_req, pieces);
+    if (s != LKV_OK) return s;
+    *bytes = sp_layout(L, n_req, pieces).total;
+    return LKV_OK;
+}
+
+lkv_status lkv_chunk_scan_sp(const lkv_layer* L, const lkv_tokens* T, float scale, const float* S_init, void* out,
+                             float* S_final, int32_t pieces, void* ws, size_t ws_bytes, void* stream) {
+    return chunk_scan_sp(L, T, scale, S_init, out, S_final, pieces, reinterpret_cast<char*>(ws), ws_bytes, stream);
 }
 
 }  // extern "C"

@@ -27,6 +27,22 @@ def _t(x: Optional[np.ndarray], dtype, device) -> Optional[torch.Tensor]:
     return torch.from_numpy(np.ascontiguousarray(x)).to(device=device, dtype=dtype)
 
 
+def sp_pieces(w: I.Workload) -> int:
+    """Piece count for the sequence-parallel scan, or 0 for the serial one: split
+    the requests' streams only when their (request, head, 64-row tile) chains
+    fill less than the 256 CUs, into at most as many pieces as fill them, each
+    of at least two chunks."""
+    L = w.layer
+    chains = w.n_req * L.h_v * max(1, L.dv // 64)
+    if chains >= 256 or w.n_req == 0:
+        return 0
+    mean_chunks = w.online.n_tok / w.n_req / L.chunk
+    p = 1
+    while p * 2 * chains <= 256 and p * 2 <= mean_chunks / 2 and p * 2 <= 8:
+        p *= 2
+    return p if p > 1 else 0
+
+
 def fold_dropped_blocks(w: I.Workload):
     """Pool rows whose transition no composition of ``w`` reads: every block that
     is not at position 2..K of some request."""
@@ -119,7 +135,17 @@ class GpuWorkload:
         lkv.init_compose(self.layer, self.w.n_blk, self.B_pool, self.M_pool, self.blk_ids, self.blk_cu,
                          int(self.w.blk_cu[-1]), self.S_exact, stream)
 
-    def scan(self, S_init: Optional[torch.Tensor], stream=None):
+    def scan(self, S_init: Optional[torch.Tensor], stream=None, pieces: int = 0):
+        """The online chunk scan from S_init; with ``pieces`` > 1 the sequence-parallel
+        form (each request's stream in that many pieces), its workspace kept here."""
+        if pieces > 1:
+            need = lkv.chunk_scan_sp_workspace(self.layer, self.w.n_req, pieces)
+            ws = getattr(self, "_sp_ws", None)
+            if ws is None or ws.numel() < need:
+                self._sp_ws = ws = torch.empty(need, dtype=torch.uint8, device=self.out.device)
+            lkv.chunk_scan_sp(self.layer, self.online.struct, self.w.scale, S_init, self.out, self.S_final, pieces,
+                              ws, stream)
+            return
         if self.w.layer.family == I.GDN:
             lkv.gdn_chunk_scan(self.layer, self.online.struct, self.w.scale, S_init, self.out, self.S_final,
                                stream)

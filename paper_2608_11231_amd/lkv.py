@@ -51,7 +51,8 @@ EXPORTS = ("lkv_abi_version", "lkv_status_string", "lkv_last_hip_error", "lkv_bl
            "lkv_init_single", "lkv_init_compose", "lkv_gdn_chunk_scan", "lkv_ssd_chunk_scan",
            "lkv_gdn_decode", "lkv_ssd_decode", "lkv_gather_selected", "lkv_init_single_bf16",
            "lkv_init_compose_bf16", "lkv_round_bf16", "lkv_stage_rows", "lkv_state_rel_error",
-           "lkv_chunk_scan_from_pool", "lkv_set_wait_limit")
+           "lkv_chunk_scan_from_pool", "lkv_set_wait_limit", "lkv_chunk_scan_sp_workspace",
+           "lkv_chunk_scan_sp")
 
 
 def load() -> ctypes.CDLL:
@@ -70,6 +71,8 @@ def load() -> ctypes.CDLL:
             lib.lkv_status_string.argtypes = [ctypes.c_int]
             lib.lkv_last_hip_error.restype = ctypes.c_int
             lib.lkv_set_wait_limit.argtypes = [i32]
+            lib.lkv_chunk_scan_sp_workspace.argtypes = [LP, i32, i32, ctypes.POINTER(ctypes.c_size_t)]
+            lib.lkv_chunk_scan_sp.argtypes = [LP, TP, f32, vp, vp, vp, i32, vp, ctypes.c_size_t, vp]
             lib.lkv_set_wait_limit.restype = i32
             lib.lkv_block_summary.argtypes = [LP, TP, vp, vp, vp]
             lib.lkv_init_single.argtypes = [LP, i32, i32, vp, vp, vp, vp]
@@ -264,3 +267,21 @@ def set_wait_limit(polls: int) -> int:
     up, negative = the default).  A wait that gives up makes the results NaN.
     Returns the previous bound."""
     return int(load().lkv_set_wait_limit(int(polls)))
+
+
+def chunk_scan_sp_workspace(layer: Layer, n_req: int, pieces: int) -> int:
+    """Workspace bytes of chunk_scan_sp."""
+    n = ctypes.c_size_t(0)
+    _check(load().lkv_chunk_scan_sp_workspace(ctypes.byref(layer), int(n_req), int(pieces), ctypes.byref(n)),
+           "lkv_chunk_scan_sp_workspace")
+    return int(n.value)
+
+
+def chunk_scan_sp(layer: Layer, online: Tokens, scale: float, S_init: Optional[torch.Tensor],
+                  out: Optional[torch.Tensor], S_final: Optional[torch.Tensor], pieces: int, ws: torch.Tensor,
+                  stream=None) -> None:
+    """The chunk scan with each request's stream split into ``pieces`` pieces
+    (sequence parallel); ``ws`` is a device workspace tensor."""
+    _check(load().lkv_chunk_scan_sp(ctypes.byref(layer), ctypes.byref(online), float(scale), _ptr(S_init), _ptr(out),
+                                    _ptr(S_final), int(pieces), _ptr(ws), int(ws.numel() * ws.element_size()),
+                                    _stream(stream)), "lkv_chunk_scan_sp")

@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_strings(lib):
-    assert lib.lkv_abi_version() == 7
+    assert lib.lkv_abi_version() == 8
     assert lib.lkv_status_string(0) == b"ok"
     assert b"NULL" in lib.lkv_status_string(1)
 
@@ -51,6 +51,25 @@ def test_wait_limit_setter(lib):
     assert lib.lkv_set_wait_limit(5) == 0
     assert lib.lkv_set_wait_limit(-3) == 5
     assert lib.lkv_set_wait_limit(-1) == default
+
+
+def test_sp_workspace_size(lib):
+    """The sequence-parallel scan's workspace: every region of the documented
+    layout, each 256-byte aligned; piece counts outside 1..64 are rejected."""
+    from paper_2608_11231_amd import lkv
+    up = lambda x: (x + 255) // 256 * 256
+    for fam, hq, hv, dk, dv, n_req, P in ((0, 2, 4, 128, 128, 3, 4), (1, 1, 64, 128, 64, 1, 8)):
+        L = _layer(family=fam, h_qk=hq, h_v=hv, dk=dk, dv=dv, gate_dtype=0 if fam else 1)
+        n = ctypes.c_size_t(0)
+        assert lib.lkv_chunk_scan_sp_workspace(ctypes.byref(L), n_req, P, ctypes.byref(n)) == 0
+        seg, state = n_req * P, hv * dv * dk * 4
+        trans = hv * dk * dk * 4 if fam == 0 else hv * 4
+        want = (up((seg + 1) * 4) + up(n_req * (P + 1) * 4) + up((n_req + 1) * 4) + up((seg + n_req) * state)
+                + up((seg + n_req) * trans) + up(seg * state) + up(n_req * state))
+        assert n.value == want
+        assert lkv.chunk_scan_sp_workspace(L, n_req, P) == want
+        for bad in (0, 65):
+            assert lib.lkv_chunk_scan_sp_workspace(ctypes.byref(L), n_req, bad, ctypes.byref(n)) == 2
 
 
 def _layer(**kw):
