@@ -44,7 +44,7 @@
 extern "C" {
 #endif
 
-#define LKV_ABI_VERSION 8
+#define LKV_ABI_VERSION 9
 
 typedef enum {
     LKV_OK = 0,
@@ -53,6 +53,7 @@ typedef enum {
     LKV_E_DTYPE = 3,        /* unknown or unsupported dtype for this argument        */
     LKV_E_ALIGN = 4,        /* a tensor pointer is not 16-byte aligned               */
     LKV_E_UNSUPPORTED = 5,  /* a valid geometry this build does not implement        */
+    LKV_E_WORKSPACE = 6,    /* beyond the allocation-free variant's fixed scratch     */
     LKV_E_HIP = 7           /* the HIP runtime reported an error (lkv_last_hip_error) */
 } lkv_status;
 
@@ -233,6 +234,26 @@ lkv_status lkv_chunk_scan_sp_workspace(const lkv_layer* layer, int32_t n_req, in
 lkv_status lkv_chunk_scan_sp(const lkv_layer* layer, const lkv_tokens* online, float scale,
                              const float* S_init, void* out, float* S_final, int32_t pieces,
                              void* ws, size_t ws_bytes, void* stream);
+
+/* Allocation-free variant of lkv_chunk_scan_sp, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): the same kernels and results, bit for
+ * bit, with the workspace taken from a fixed scratch array of 64 MiB that the
+ * library's device code holds on every GPU it runs on until the process ends.
+ * The call allocates and frees nothing.  Arguments as in lkv_chunk_scan_sp,
+ * without the workspace; a call whose workspace (lkv_chunk_scan_sp_workspace)
+ * exceeds 64 MiB returns LKV_E_WORKSPACE and launches nothing (at dk = dv =
+ * 128 and 32 heads a state takes 2 MiB, so e.g. one request in up to 6
+ * pieces fits, Mamba-2 with 64 heads of 64 x 128 one request in up to 15).
+ * Every call on a GPU shares that GPU's array: calls that overlap on one GPU
+ * (on different streams, or from several threads) race and must be ordered
+ * by the caller.  No part of the array needs clearing between calls (every
+ * byte a call reads it has first written).  The first call on a device, with
+ * that device current, looks up the array's device address (no allocation).
+ * Errors: as lkv_chunk_scan_sp, and LKV_E_WORKSPACE. */
+lkv_status lkv_chunk_scan_sp_noalloc(const lkv_layer* layer, const lkv_tokens* online, float scale,
+                                     const float* S_init, void* out, float* S_final, int32_t pieces,
+                                     void* stream);
 
 /* Decode step: the step that follows the online prefill, which keeps only the
  * final state for it (Sec. 2).  One new token per request advances each

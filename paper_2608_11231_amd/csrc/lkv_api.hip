@@ -3,6 +3,7 @@
 #include <stdlib.h>
 
 #include <atomic>
+#include <mutex>
 
 #include "decode_kernels.h"
 #include "diag_kernels.h"
@@ -308,6 +309,35 @@ lkv_status chunk_scan_sp(const lkv_layer* L, const lkv_tokens* T, float scale, c
     return chunk_scan(L, &Tp, L->family == LKV_GDN ? scale : 1.f, S_start, out, nullptr, stream);
 }
 
+// Scratch of the allocation-free sequence-parallel scan: one fixed array per
+// GPU, in the library's device code, held until the process ends.  Host code
+// never uses the array's name (on the host it is only a stand-in for the
+// symbol): its device address is taken once per device with
+// hipGetSymbolAddress, with that device current, and kept here.
+constexpr size_t kScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+lkv_status scratch_for_current_device(char** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_status(e);
+    if (dev < 0 || dev >= kMaxDevices) return LKV_E_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_status(e);
+        if (!ptr) return LKV_E_HIP;
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = reinterpret_cast<char*>(g_scratch_ptr[dev]);
+    return LKV_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -322,6 +352,7 @@ const char* lkv_status_string(lkv_status s) {
         case LKV_E_DTYPE: return "unsupported dtype";
         case LKV_E_ALIGN: return "tensor pointer not 16-byte aligned";
         case LKV_E_UNSUPPORTED: return "geometry not implemented by this build";
+        case LKV_E_WORKSPACE: return "needs more scratch than the allocation-free variant's fixed 64 MiB per GPU";
         case LKV_E_HIP: return "HIP runtime error";
     }
     return "unknown status";
@@ -527,6 +558,18 @@ lkv_status lkv_chunk_scan_sp_workspace(const lkv_layer* L, int32_t n_req, int32_
 lkv_status lkv_chunk_scan_sp(const lkv_layer* L, const lkv_tokens* T, float scale, const float* S_init, void* out,
                              float* S_final, int32_t pieces, void* ws, size_t ws_bytes, void* stream) {
     return chunk_scan_sp(L, T, scale, S_init, out, S_final, pieces, reinterpret_cast<char*>(ws), ws_bytes, stream);
+}
+
+lkv_status lkv_chunk_scan_sp_noalloc(const lkv_layer* L, const lkv_tokens* T, float scale, const float* S_init,
+                                     void* out, float* S_final, int32_t pieces, void* stream) {
+    if (!T) return LKV_E_NULL;
+    lkv_status s = sp_check(L, T->n_seq, pieces);
+    if (s != LKV_OK) return s;
+    if (sp_layout(L, T->n_seq, pieces).total > kScratchBytes) return LKV_E_WORKSPACE;
+    char* ws = nullptr;
+    s = scratch_for_current_device(&ws);
+    if (s != LKV_OK) return s;
+    return chunk_scan_sp(L, T, scale, S_init, out, S_final, pieces, ws, kScratchBytes, stream);
 }
 
 }  // extern "C"

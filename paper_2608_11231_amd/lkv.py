@@ -21,7 +21,7 @@ GDN, SSD = 0, 1
 F32, BF16 = 0, 1
 
 _STATUS = {0: "LKV_OK", 1: "LKV_E_NULL", 2: "LKV_E_SHAPE", 3: "LKV_E_DTYPE", 4: "LKV_E_ALIGN",
-           5: "LKV_E_UNSUPPORTED", 7: "LKV_E_HIP"}
+           5: "LKV_E_UNSUPPORTED", 6: "LKV_E_WORKSPACE", 7: "LKV_E_HIP"}
 
 
 class LkvError(RuntimeError):
@@ -52,7 +52,7 @@ EXPORTS = ("lkv_abi_version", "lkv_status_string", "lkv_last_hip_error", "lkv_bl
            "lkv_gdn_decode", "lkv_ssd_decode", "lkv_gather_selected", "lkv_init_single_bf16",
            "lkv_init_compose_bf16", "lkv_round_bf16", "lkv_stage_rows", "lkv_state_rel_error",
            "lkv_chunk_scan_from_pool", "lkv_set_wait_limit", "lkv_chunk_scan_sp_workspace",
-           "lkv_chunk_scan_sp")
+           "lkv_chunk_scan_sp", "lkv_chunk_scan_sp_noalloc")
 
 
 def load() -> ctypes.CDLL:
@@ -73,6 +73,7 @@ def load() -> ctypes.CDLL:
             lib.lkv_set_wait_limit.argtypes = [i32]
             lib.lkv_chunk_scan_sp_workspace.argtypes = [LP, i32, i32, ctypes.POINTER(ctypes.c_size_t)]
             lib.lkv_chunk_scan_sp.argtypes = [LP, TP, f32, vp, vp, vp, i32, vp, ctypes.c_size_t, vp]
+            lib.lkv_chunk_scan_sp_noalloc.argtypes = [LP, TP, f32, vp, vp, vp, i32, vp]
             lib.lkv_set_wait_limit.restype = i32
             lib.lkv_block_summary.argtypes = [LP, TP, vp, vp, vp]
             lib.lkv_init_single.argtypes = [LP, i32, i32, vp, vp, vp, vp]
@@ -285,3 +286,12 @@ def chunk_scan_sp(layer: Layer, online: Tokens, scale: float, S_init: Optional[t
     _check(load().lkv_chunk_scan_sp(ctypes.byref(layer), ctypes.byref(online), float(scale), _ptr(S_init), _ptr(out),
                                     _ptr(S_final), int(pieces), _ptr(ws), int(ws.numel() * ws.element_size()),
                                     _stream(stream)), "lkv_chunk_scan_sp")
+
+
+def chunk_scan_sp_noalloc(layer: Layer, online: Tokens, scale: float, S_init: Optional[torch.Tensor],
+                          out: Optional[torch.Tensor], S_final: Optional[torch.Tensor], pieces: int,
+                          stream=None) -> None:
+    """chunk_scan_sp on the library's fixed per-GPU scratch (allocates nothing)."""
+    _check(load().lkv_chunk_scan_sp_noalloc(ctypes.byref(layer), ctypes.byref(online), float(scale), _ptr(S_init),
+                                            _ptr(out), _ptr(S_final), int(pieces), _stream(stream)),
+           "lkv_chunk_scan_sp_noalloc")

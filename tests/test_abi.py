@@ -37,7 +37,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_version_and_strings(lib):
-    assert lib.lkv_abi_version() == 8
+    assert lib.lkv_abi_version() == 9
     assert lib.lkv_status_string(0) == b"ok"
     assert b"NULL" in lib.lkv_status_string(1)
 
