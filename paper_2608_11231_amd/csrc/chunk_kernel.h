@@ -1010,6 +1010,9 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
 hipError_t launch_scan_gdn(int dk, int chunk, bool f32io, const ScanArgs& a, hipStream_t st);
 hipError_t launch_scan_ssd(int dk, int chunk, bool f32io, const ScanArgs& a, hipStream_t st);
 size_t scan_lds_bytes(int fam, int dk, int chunk, bool f32io, int nb, bool summary);
+// Mamba-2 scan / block-summary kernel with four symmetric state waves (ssd_scan.hip)
+bool ssd_scan_supported(int dk, int chunk, bool f32io, int dv);
+hipError_t launch_ssd_scan(int dk, const ScanArgs& a, hipStream_t st);
 
 template <int FAM, int DK, int CH, bool F32IO, int NB, bool SUMMARY, int RT = 1>
 hipError_t launch_chunk_nb(const ScanArgs& a, hipStream_t st) {

@@ -112,6 +112,25 @@ ScanArgs base_args(const lkv_layer* L, const lkv_tokens* T) {
     return a;
 }
 
+// Mamba-2 scans and block summaries can run on ssd_scan_kernel where it
+// covers the shapes (bf16 io, 64-token chunks, dk >= 32, dv a multiple of 64):
+// LKV_SSD_SCAN_KERNEL=1 selects it, otherwise the shared chunk kernel runs
+// (the two give identical bits).
+bool use_ssd_scan(const lkv_layer* L) {
+    return L->family == LKV_SSD && env_int("LKV_SSD_SCAN_KERNEL", 0) == 1 &&
+           ssd_scan_supported(L->dk, L->chunk, L->io_dtype == LKV_F32, L->dv);
+}
+
+lkv_status ssd_scan(const lkv_layer* L, ScanArgs a, int64_t pairs, hipStream_t st) {
+    const int64_t units = pairs * (L->dv / 64);
+    if (units >= (INT64_C(1) << 31)) return LKV_E_SHAPE;
+    a.tiles_b = L->dv / 64;
+    a.tiles_m = 0;
+    a.nb = 4;
+    a.n_units = (int32_t)units;
+    return hip_status(launch_ssd_scan(L->dk, a, st));
+}
+
 hipError_t launch_scan(const lkv_layer* L, const ScanArgs& a, hipStream_t st) {
     const bool f32io = L->io_dtype == LKV_F32;
     return L->family == LKV_GDN ? launch_scan_gdn(L->dk, L->chunk, f32io, a, st)
@@ -128,10 +147,6 @@ lkv_status chunk_scan(const lkv_layer* L, const lkv_tokens* T, float scale, cons
     if (!out && !S_final) return LKV_OK;
     const bool f32io = L->io_dtype == LKV_F32;
     const int64_t pairs = (int64_t)T->n_seq * L->h_v;
-    const int nw = pick_nw(L->family, L->dk, L->chunk, f32io, pairs, L->dv, 0, false);
-    if (nw == 0) return LKV_E_UNSUPPORTED;
-    const int64_t units = pairs * (L->dv / (16 * nw));
-    if (units >= (INT64_C(1) << 31)) return LKV_E_SHAPE;
     ScanArgs a = base_args(L, T);
     a.scale = scale;
     a.S_init = S_init;
@@ -141,6 +156,11 @@ lkv_status chunk_scan(const lkv_layer* L, const lkv_tokens* T, float scale, cons
     a.out = out;
     a.S_final = S_final;
     a.summary = 0;
+    if (use_ssd_scan(L)) return ssd_scan(L, a, pairs, (hipStream_t)stream);
+    const int nw = pick_nw(L->family, L->dk, L->chunk, f32io, pairs, L->dv, 0, false);
+    if (nw == 0) return LKV_E_UNSUPPORTED;
+    const int64_t units = pairs * (L->dv / (16 * nw));
+    if (units >= (INT64_C(1) << 31)) return LKV_E_SHAPE;
     a.tiles_b = L->dv / (16 * nw);
     a.tiles_m = 0;
     a.nb = nw;
@@ -392,6 +412,7 @@ lkv_status lkv_block_summary(const lkv_layer* L, const lkv_tokens* T, float* B_o
         return hip_status(launch_ssd_lambda(T->cu, T->n_seq, T->n_tok, L->h_v, reinterpret_cast<const float*>(T->g),
                                             T->A, M_out, st));
     }
+    if (use_ssd_scan(L)) return ssd_scan(L, a, pairs, st);
     const int nw = pick_nw(L->family, L->dk, L->chunk, f32io, pairs, rows_b ? rows_b : rows_m,
                            rows_b ? rows_m : 0, true);
     if (nw == 0) return LKV_E_UNSUPPORTED;

@@ -52,6 +52,10 @@ SSD_CASES = [
     (128, 64, 64, "bf16", 1, 4, ((130, 64), (1, 70)), (150, 64)),
     (64, 32, 16, "bf16", 2, 4, ((50,),), (77,)),
     (64, 64, 16, "f32", 1, 2, ((20,),), (33,)),
+    # other state widths with 64-token chunks: grouped B / C, ragged and empty segments
+    (32, 64, 64, "bf16", 2, 4, ((100, 0, 65),), (129,)),
+    (64, 128, 64, "bf16", 1, 2, ((64, 128), (3,)), (0, 191)),
+    # the largest supported state (N = 128, P = 512); kept last (the pinned-geometry test takes it)
     (128, 512, 64, "bf16", 1, 2, ((70,),), (90,)),
 ]
 
