@@ -82,6 +82,14 @@ struct ScanArgs {
     int32_t nb;           // B-waves per workgroup (16*nb rows per tile)
     int32_t n_units;
     int32_t wait_limit;   // polls of the solver's bounded wait for the stagers' signals
+    // Mamba-2 scan kernel only: with pieces > 1 every segment is cut into that
+    // many pieces of whole chunks (the sequence-parallel scan's cut), piece 0
+    // starting from the segment's initial state and the others from zero;
+    // every piece's end state and log-decay sum go to piece_B / piece_L
+    // ([n_seq * pieces, h_v, dv, dk] / [n_seq * pieces, h_v]) instead of S_final
+    int32_t pieces;
+    float* piece_B;
+    float* piece_L;
 };
 
 template <int FAM, int DK, int CH, bool F32IO, int NB, bool SUMMARY>
@@ -1010,9 +1018,27 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
 hipError_t launch_scan_gdn(int dk, int chunk, bool f32io, const ScanArgs& a, hipStream_t st);
 hipError_t launch_scan_ssd(int dk, int chunk, bool f32io, const ScanArgs& a, hipStream_t st);
 size_t scan_lds_bytes(int fam, int dk, int chunk, bool f32io, int nb, bool summary);
-// Mamba-2 scan / block-summary kernel with four symmetric state waves (ssd_scan.hip)
+// Mamba-2 scan / block-summary kernel with eight symmetric state waves, and
+// the output correction of its pieces (ssd_scan.hip)
 bool ssd_scan_supported(int dk, int chunk, bool f32io, int dv);
 hipError_t launch_ssd_scan(int dk, const ScanArgs& a, hipStream_t st);
+struct SsdCorrectArgs {
+    const int32_t* cu;     // the requests' token ranges (as the scan's cu)
+    int32_t n_seq;
+    int64_t n_tok;
+    const void* C;         // [n_tok, h_qk, dk] bf16
+    const float* dt;       // [n_tok, h_v]
+    const float* A;        // [h_v]
+    int32_t h_qk, h_v, dv, pieces;
+    const float* piece_B;  // the pieces' end states and log-decay sums (ScanArgs::piece_B / piece_L)
+    const float* piece_L;
+    void* y;               // [n_tok, h_v, dv] bf16: piece outputs from zero, corrected in place; or null
+    float* S_final;        // [n_seq, h_v, dv, dk] or null
+    int32_t tiles;         // 64-row tiles over dv
+    int32_t slots;         // chunk slots per piece (1..8): slot j takes chunks j, j + slots, ...
+    int32_t n_units;
+};
+hipError_t launch_ssd_correct(int dk, const SsdCorrectArgs& a, hipStream_t st);
 
 template <int FAM, int DK, int CH, bool F32IO, int NB, bool SUMMARY, int RT = 1>
 hipError_t launch_chunk_nb(const ScanArgs& a, hipStream_t st) {

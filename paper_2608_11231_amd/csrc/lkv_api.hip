@@ -121,6 +121,14 @@ bool use_ssd_scan(const lkv_layer* L) {
            ssd_scan_supported(L->dk, L->chunk, L->io_dtype == LKV_F32, L->dv);
 }
 
+// The sequence-parallel Mamba-2 scan as one pass over the pieces plus an
+// output correction, on the same shapes; LKV_SSD_SP_CORRECT=0 selects the
+// summary / composition / rescan form shared with Gated DeltaNet.
+bool use_ssd_sp(const lkv_layer* L) {
+    return L->family == LKV_SSD && env_int("LKV_SSD_SP_CORRECT", 1) == 1 &&
+           ssd_scan_supported(L->dk, L->chunk, L->io_dtype == LKV_F32, L->dv);
+}
+
 lkv_status ssd_scan(const lkv_layer* L, ScanArgs a, int64_t pairs, hipStream_t st) {
     const int64_t units = pairs * (L->dv / 64);
     if (units >= (INT64_C(1) << 31)) return LKV_E_SHAPE;
@@ -309,6 +317,54 @@ lkv_status chunk_scan_sp(const lkv_layer* L, const lkv_tokens* T, float scale, c
     float* S_start = reinterpret_cast<float*>(ws + ly.S_start);
     float* S_last = S_final ? S_final : reinterpret_cast<float*>(ws + ly.S_last);
     const int64_t state = (int64_t)L->h_v * L->dv * L->dk;
+    if (pieces > 1 && use_ssd_sp(L)) {
+        // Mamba-2: the pieces scanned once, piece 0 from the initial state and
+        // the others from zero, then their outputs corrected and the final
+        // state composed (ssd_correct_kernel)
+        const int tiles = L->dv / 64;
+        const int64_t units = (int64_t)n_seg * L->h_v * tiles;
+        if (units >= (INT64_C(1) << 31)) return LKV_E_SHAPE;
+        ScanArgs a = base_args(L, T);
+        a.S_init = S_init;
+        a.out = out;
+        a.summary = 0;
+        a.tiles_b = tiles;
+        a.nb = 4;
+        a.n_units = (int32_t)units;
+        a.pieces = pieces;
+        a.piece_B = Bp;
+        a.piece_L = Mp;
+        lkv_status e = hip_status(launch_ssd_scan(L->dk, a, st));
+        if (e != LKV_OK) return e;
+        SsdCorrectArgs c = {};
+        c.cu = T->cu;
+        c.n_seq = n_req;
+        c.n_tok = T->n_tok;
+        c.C = T->q;
+        c.dt = reinterpret_cast<const float*>(T->g);
+        c.A = T->A;
+        c.h_qk = L->h_qk;
+        c.h_v = L->h_v;
+        c.dv = L->dv;
+        c.pieces = pieces;
+        c.piece_B = Bp;
+        c.piece_L = Mp;
+        c.y = out;
+        c.S_final = S_final;
+        c.tiles = tiles;
+        // chunk slots: about one workgroup per CU, at most a piece's chunks
+        // (ceil(ceil(n_tok / P) / CH) bounds them) and at most 8
+        const int64_t max_chunks = ((T->n_tok + pieces - 1) / pieces + L->chunk - 1) / L->chunk;
+        const int64_t base = (int64_t)n_req * (pieces - 1) * L->h_v * tiles;
+        int64_t slots = (256 + base - 1) / base;
+        if (slots > max_chunks) slots = max_chunks;
+        if (env_int("LKV_SSD_CORRECT_SLOTS", 0) > 0) slots = env_int("LKV_SSD_CORRECT_SLOTS", 0);
+        c.slots = (int32_t)(slots < 1 ? 1 : (slots > 8 ? 8 : slots));
+        const int64_t cunits = (int64_t)n_req * (pieces - 1) * L->h_v * tiles * c.slots;
+        if (cunits >= (INT64_C(1) << 31)) return LKV_E_SHAPE;
+        c.n_units = (int32_t)cunits;
+        return hip_status(launch_ssd_correct(L->dk, c, st));
+    }
     lkv_status e = hip_status(launch_sp_setup(T->cu, n_req, pieces, L->chunk, T->n_tok, piece_cu, blk_ids, blk_cu,
                                               S_init, Bp + (int64_t)n_seg * state, state, st));
     if (e != LKV_OK) return e;

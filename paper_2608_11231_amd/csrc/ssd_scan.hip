@@ -28,6 +28,17 @@
 
 namespace lkv {
 
+// Piece pc of P of the token range [t0, t1): pieces of whole chunks, ceil(len /
+// P) tokens rounded up to a chunk multiple each; the last pieces take what is
+// left and may be empty (the sequence-parallel scan's cut).
+__device__ __forceinline__ void piece_range(int64_t& t0, int64_t& t1, int P, int pc, int CH) {
+    const int64_t len = t1 - t0;
+    const int64_t per = ((len + P - 1) / P + CH - 1) / CH * CH;
+    const int64_t a = (int64_t)pc * per, b = a + per;
+    t1 = t0 + (b < len ? b : len);
+    t0 = t0 + (a < len ? a : len);
+}
+
 template <int DK>
 struct SsdLds {
     static constexpr int CH = 64, NTC = 4, NTK = DK / 16, NH = NTK / 2;
@@ -68,13 +79,16 @@ __global__ __launch_bounds__(512) void ssd_scan_kernel(ScanArgs p) {
     const int u = xcd_unit(blockIdx.x, p.n_units);
     const int tile = u % tiles;
     const int h = (u / tiles) % p.h_v;
-    const int s = u / (tiles * p.h_v);
+    const int sp = u / (tiles * p.h_v);  // segment, or (segment, piece) with pieces > 1
+    const int P = p.pieces > 1 ? p.pieces : 1;
+    const int s = sp / P, pc = sp % P;
     const int hq = h / (p.h_v / p.h_qk);
     const int row0 = tile * 64;
     const int my_row = row0 + 16 * rt + c16;  // the state row this lane's tiles hold
     int64_t t0 = p.cu[s], t1 = p.cu[s + 1];
     t0 = t0 < 0 ? 0 : (t0 > p.n_tok ? p.n_tok : t0);
     t1 = t1 < t0 ? t0 : (t1 > p.n_tok ? p.n_tok : t1);
+    if (P > 1) piece_range(t0, t1, P, pc, CH);
     const int nch = (int)((t1 - t0 + CH - 1) / CH);
     const float Ah = p.A[h];
 
@@ -188,8 +202,8 @@ __global__ __launch_bounds__(512) void ssd_scan_kernel(ScanArgs p) {
     {
         int64_t init_row = s;
         float init_fill = 0.f;
-        bool init_load = p.S_init != nullptr;
-        if (p.src) {
+        bool init_load = p.S_init != nullptr && pc == 0;  // later pieces start from zero
+        if (p.src && pc == 0) {
             const int32_t id = p.src[s];
             init_row = id;
             if (id < 0 || id >= p.n_src) {
@@ -224,7 +238,16 @@ __global__ __launch_bounds__(512) void ssd_scan_kernel(ScanArgs p) {
             *sSh(e, NH * hf + j) = Sh[j];
         }
     };
-    if (with_out) publish(0);
+    // The initial state is used here on every path, so its loads are complete
+    // before the loop: a state register still waiting on a load at the loop
+    // head would make the loop's first use of the state wait for every load in
+    // flight -- the next chunk's prefetch included -- in every chunk.
+#pragma unroll
+    for (int j = 0; j < NH; ++j) Sh[j] = to_bf16(S[j]);
+    if (with_out) {
+#pragma unroll
+        for (int j = 0; j < NH; ++j) *sSh(0, NH * hf + j) = Sh[j];
+    }
 
     // ---- prologue: chunk 0 committed, its output blocks built; chunk 1 in flight
     if (nch > 0) {
@@ -345,12 +368,231 @@ __global__ __launch_bounds__(512) void ssd_scan_kernel(ScanArgs p) {
         if (ci + 1 < nch && with_out) p_blocks(b ^ 1);
     }
     if (p.summary && p.M_out && tile == 0 && w == 0 && lane == 0) p.M_out[int64_t(s) * p.h_v + h] = lam;
-    if (p.S_final) {
+    float* dst = P > 1 ? p.piece_B : p.S_final;
+    if (P > 1 && tile == 0 && w == 0 && lane == 0) p.piece_L[int64_t(sp) * p.h_v + h] = lam;
+    if (dst) {
 #pragma unroll
         for (int j = 0; j < NH; ++j)
-            *reinterpret_cast<f32x4*>(p.S_final + ((int64_t(s) * p.h_v + h) * p.dv + my_row) * DK +
-                                      16 * (NH * hf + j) + 4 * g) = S[j];
+            *reinterpret_cast<f32x4*>(dst + ((int64_t(sp) * p.h_v + h) * p.dv + my_row) * DK + 16 * (NH * hf + j) +
+                                      4 * g) = S[j];
     }
+}
+
+// Output correction of the sequence-parallel Mamba-2 scan.  With a scalar
+// decay per token the state at token t of piece p is exp(L_t) S_p + (the state
+// of the piece's own tokens from zero), L_t being the log-decay summed from
+// the piece's start through t (Eq. 2).  So the outputs of a piece scanned from
+// zero lack exactly exp(L_t) C_t S_p^T, and its start state S_p is Eq. 5 over
+// the earlier pieces: S_1 = (piece 0's end state, which started from the
+// request's own), S_{p+1} = exp(Lambda_p) S_p + B_p.  One workgroup per
+// (request, piece >= 1, head, 64 state rows, chunk slot j of J), four waves of
+// 16 rows: it composes S_p (slot 0 of the last piece also the final state),
+// then takes the piece's chunks j, j + J, ... adding exp(L_t) (S_p C^T) to
+// their outputs.  The slots put a piece's chunks in flight together: each
+// chunk is little work, and a workgroup waiting on one load round trip per
+// chunk would be bound by memory latency.  S_p enters the product as its bf16
+// hi part, like the state in the scan's own outputs.
+template <int DK>
+__global__ __launch_bounds__(256) void ssd_correct_kernel(SsdCorrectArgs p) {
+    constexpr int CH = 64, NTC = 4, NTK = DK / 16, SK = DK + 16, JMAX = 8;
+    extern __shared__ __align__(16) char smem[];
+    bf16* sC = reinterpret_cast<bf16*>(smem);
+    float* sE = reinterpret_cast<float*>(smem + size_t(CH) * SK * 2);  // exp(L_t) of the chunk's tokens
+    const int tid = threadIdx.x;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int lane = tid & 63, g = lane >> 4, c16 = lane & 15;
+    const int P = p.pieces, J = p.slots;
+    // unit order, innermost first: chunk slot, row tile, head, (request, piece)
+    const int u = xcd_unit(blockIdx.x, p.n_units);
+    const int j = u % J;
+    const int tile = (u / J) % p.tiles;
+    const int h = (u / (J * p.tiles)) % p.h_v;
+    const int rp = u / (J * p.tiles * p.h_v);
+    const int r = rp / (P - 1), pc = rp % (P - 1) + 1;
+    const int hq = h / (p.h_v / p.h_qk);
+    const int row0 = tile * 64;
+    const int my_row = row0 + 16 * w + c16;
+    int64_t t0 = p.cu[r], t1 = p.cu[r + 1];
+    t0 = t0 < 0 ? 0 : (t0 > p.n_tok ? p.n_tok : t0);
+    t1 = t1 < t0 ? t0 : (t1 > p.n_tok ? p.n_tok : t1);
+    piece_range(t0, t1, P, pc, CH);
+    const int nch = (int)((t1 - t0 + CH - 1) / CH);
+    const bool outputs = p.y != nullptr && j < nch;  // uniform over the workgroup
+    const bool final_state = pc == P - 1 && j == 0 && p.S_final != nullptr;
+    if (!outputs && !final_state) return;
+
+    // ---- this slot's first chunk is requested before the start state: the C
+    // tile and dt a chunk ahead in registers, the outputs being corrected too
+    KQTile<CH, DK, false, 256> pCt;
+    uint32_t pdt = 0u;  // wave 0: the chunk's dt (lane = token)
+    float pskip = 0.f;  // wave 0: dt summed over the chunks this slot skips next
+    bf16x4 py[NTC];
+    const float Ah = p.A[h];
+    const uint32_t c_rb = (uint32_t)p.h_qk * DK * 2, g_rb = (uint32_t)p.h_v * 4;
+    const int64_t ycol_w = (int64_t)h * p.dv + row0 + 16 * w;  // the wave's first output row (uniform)
+    const int64_t ycol = ycol_w + 4 * g;
+    // dt of the piece's tokens from t0: zero past the piece
+    const __amdgpu_buffer_rsrc_t rdt =
+        make_rsrc(reinterpret_cast<const char*>(p.dt) + (t0 * p.h_v + h) * 4, (uint32_t)(t1 - t0) * g_rb);
+    auto prefetch = [&](int ci) {
+        const int64_t c0 = t0 + (int64_t)ci * CH;
+        const uint32_t n = (uint32_t)((t1 - c0) < CH ? (t1 - c0) : CH);
+        pCt.load_buf(make_rsrc(reinterpret_cast<const char*>(p.C) + (c0 * p.h_qk + hq) * (int64_t)DK * 2, n * c_rb), 0u,
+                     c_rb, tid);
+        if (w == 0) {
+            pdt = buf_load4(rdt, (uint32_t)(ci * CH + lane) * g_rb);
+            float acc = 0.f;
+#pragma unroll
+            for (int k = 1; k < JMAX; ++k) {
+                const uint32_t off = k < J ? (uint32_t)((ci + k) * CH + lane) * g_rb : 0xffffffffu;
+                acc += __builtin_bit_cast(float, buf_load4(rdt, off));
+            }
+            pskip = acc;
+        }
+        // this lane's outputs: 4 rows of token 16mt + c16 (zeros past the piece);
+        // the resource's base is the wave's (uniform), the lane's rows in the offset
+        const uint32_t y_rb = (uint32_t)p.h_v * p.dv * 2;
+        const __amdgpu_buffer_rsrc_t ry =
+            make_rsrc(reinterpret_cast<const char*>(p.y) + (c0 * p.h_v * (int64_t)p.dv + ycol_w) * 2, n * y_rb);
+#pragma unroll
+        for (int mt = 0; mt < NTC; ++mt) {
+            const uint32_t t = 16 * mt + c16;
+            const uint32_t off = t < n ? t * y_rb + 8 * g : 0xffffffffu;
+            py[mt] = __builtin_bit_cast(bf16x4, __builtin_amdgcn_raw_buffer_load_b64(ry, off, 0, 0));
+        }
+    };
+    float Lrun = 0.f;  // wave 0: A_h times the piece's dt before the current chunk
+    if (outputs) {
+        prefetch(j);
+        if (w == 0) {
+            // the chunks before this slot's first one (j < JMAX), all requested at once
+            float acc = 0.f;
+#pragma unroll
+            for (int k = 0; k < JMAX - 1; ++k) {
+                const uint32_t off = k < j ? (uint32_t)(k * CH + lane) * g_rb : 0xffffffffu;
+                acc += __builtin_bit_cast(float, buf_load4(rdt, off));
+            }
+            Lrun = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, wave_incl_scan(Ah * acc)),
+                                                                          CH - 1));
+        }
+    }
+
+    // ---- the piece's start state (acc layout: S[nt] holds S[my_row][16nt + 4g + r])
+    // as the weighted sum S_p = sum_q exp(Lambda_{q+1} + ... + Lambda_{p-1}) B_q,
+    // four pieces' states requested at a time (one load round trip for p <= 4)
+    auto brow = [&](int q) {
+        return p.piece_B + ((int64_t(r) * P + q) * p.h_v + h) * (int64_t)p.dv * DK + (int64_t)my_row * DK + 4 * g;
+    };
+    auto lam = [&](int q) { return p.piece_L[(int64_t(r) * P + q) * p.h_v + h]; };
+    // lane q: the log-weight of piece q's state (pieces past pc: unused)
+    float lw;
+    {
+        const float x = (lane >= 1 && lane < pc) ? lam(lane) : 0.f;
+        const float pre = wave_incl_scan(x);
+        const float tot = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, pre), CH - 1));
+        lw = tot - pre;
+    }
+    f32x4 S[NTK];
+#pragma unroll
+    for (int nt = 0; nt < NTK; ++nt) S[nt] = zero4();
+    for (int q0 = 0; q0 < pc; q0 += 4) {  // pc <= P - 1 < 64
+        f32x4 bl[4][NTK];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if (q0 + i >= pc) break;  // uniform
+            const float* bq = brow(q0 + i);
+#pragma unroll
+            for (int nt = 0; nt < NTK; ++nt) bl[i][nt] = *reinterpret_cast<const f32x4*>(bq + 16 * nt);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if (q0 + i >= pc) break;  // uniform
+            const float e = __expf(__builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, lw),
+                                                                                         q0 + i)));
+#pragma unroll
+            for (int nt = 0; nt < NTK; ++nt) S[nt] += e * bl[i][nt];
+        }
+    }
+    if (final_state) {
+        const float e = __expf(lam(pc));
+        const float* bq = brow(pc);
+        float* sf = p.S_final + ((int64_t(r) * p.h_v + h) * p.dv + my_row) * DK + 4 * g;
+        f32x4 bl[NTK];  // every load in flight before the first store
+#pragma unroll
+        for (int nt = 0; nt < NTK; ++nt) bl[nt] = *reinterpret_cast<const f32x4*>(bq + 16 * nt);
+#pragma unroll
+        for (int nt = 0; nt < NTK; ++nt) *reinterpret_cast<f32x4*>(sf + 16 * nt) = e * S[nt] + bl[nt];
+    }
+    if (!outputs) return;
+    bf16x4 Sh[NTK];
+#pragma unroll
+    for (int nt = 0; nt < NTK; ++nt) Sh[nt] = to_bf16(S[nt]);
+
+    for (int ci = j; ci < nch; ci += J) {
+        const int64_t c0 = t0 + (int64_t)ci * CH;
+        const int n = (int)((t1 - c0) < CH ? (t1 - c0) : CH);
+        lds_barrier();  // the previous chunk's tile is no longer read
+        pCt.commit(sC, SK, 0, tid);
+        if (w == 0) {
+            const float l = wave_incl_scan(Ah * __builtin_bit_cast(float, pdt));  // zero dt past the piece
+            sE[lane] = __expf(Lrun + l);
+            const float skip = wave_incl_scan(Ah * pskip);
+            Lrun += __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, l), CH - 1)) +
+                    __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, skip), CH - 1));
+        }
+        bf16x4 yv[NTC];
+#pragma unroll
+        for (int mt = 0; mt < NTC; ++mt) yv[mt] = py[mt];
+        if (ci + J < nch) prefetch(ci + J);
+        lds_barrier();
+        // y^T tile mt (rows 16w + 4g + j, tokens 16mt + c16) += exp(L_t) S_hi C^T
+        constexpr int NKP = NTK / 2;
+        bf16x8 cf[NKP][NTC];
+#pragma unroll
+        for (int kp = 0; kp < NKP; ++kp)
+#pragma unroll
+            for (int mt = 0; mt < NTC; ++mt) cf[kp][mt] = lds8(sC + (16 * mt + c16) * SK + 32 * kp + 8 * g);
+        float el[NTC];
+#pragma unroll
+        for (int mt = 0; mt < NTC; ++mt) el[mt] = sE[16 * mt + c16];
+        __builtin_amdgcn_sched_barrier(0);
+        f32x4 OT[NTC];
+#pragma unroll
+        for (int mt = 0; mt < NTC; ++mt) OT[mt] = zero4();
+#pragma unroll
+        for (int kp = 0; kp < NKP; ++kp)
+#pragma unroll
+            for (int mt = 0; mt < NTC; ++mt) OT[mt] = mma32(Sh[2 * kp], Sh[2 * kp + 1], cf[kp][mt], OT[mt]);
+#pragma unroll
+        for (int mt = 0; mt < NTC; ++mt) {
+            const int t = 16 * mt + c16;
+            if (t < n) {
+                const int64_t oi = (c0 + t) * p.h_v * (int64_t)p.dv + ycol;
+                *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(p.y) + oi) =
+                    to_bf16(to_f32(yv[mt]) + el[mt] * OT[mt]);
+            }
+        }
+    }
+}
+
+template <int DK>
+static hipError_t launch_ssd_correct_t(const SsdCorrectArgs& a, hipStream_t st) {
+    const size_t lds = size_t(64) * (DK + 16) * 2 + 64 * 4;
+    auto kern = ssd_correct_kernel<DK>;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kern, dim3(a.n_units), dim3(256), lds, st, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_ssd_correct(int dk, const SsdCorrectArgs& a, hipStream_t st) {
+    switch (dk) {
+        case 32: return launch_ssd_correct_t<32>(a, st);
+        case 64: return launch_ssd_correct_t<64>(a, st);
+        case 128: return launch_ssd_correct_t<128>(a, st);
+    }
+    return hipErrorInvalidValue;
 }
 
 template <int DK>

@@ -126,7 +126,10 @@ def test_scan_from_pool_matches_chunk_kernel(bf16_pool):
 
 
 @pytest.mark.parametrize("pieces", [2, 4])
-def test_sequence_parallel_matches_chunk_kernel(pieces):
+def test_sequence_parallel_matches_chunk_kernel(pieces, monkeypatch):
+    """The summary / composition / rescan form of the sequence-parallel scan,
+    on either kernel."""
+    monkeypatch.setenv("LKV_SSD_SP_CORRECT", "0")
     w = _work(CASES[3])
     G = gpu_io.GpuWorkload(w, with_cached=False)
     rng = np.random.default_rng(9)
@@ -139,3 +142,47 @@ def test_sequence_parallel_matches_chunk_kernel(pieces):
     o_ref, S_ref = R.scan(w, S0.cpu().numpy())
     assert rel_slices(S.cpu().numpy(), S_ref) < 1e-4
     assert max_abs(out.float().cpu().numpy(), o_ref) < 2e-2
+
+
+SP_CASES = [
+    # (N, P, G, H, online lengths): ragged, empty, one-token and chunk-multiple requests
+    (128, 64, 1, 4, (450, 63, 0, 200)),
+    (64, 128, 2, 4, (333, 64, 1, 640)),
+    (32, 192, 1, 2, (1000,)),
+]
+
+
+@pytest.mark.parametrize("with_out", [True, False])
+@pytest.mark.parametrize("with_init", [True, False])
+@pytest.mark.parametrize("pieces", [2, 3, 4, 8])
+@pytest.mark.parametrize("case", SP_CASES, ids=[f"ssd{c[:4]}" for c in SP_CASES])
+def test_sequence_parallel_correction(case, pieces, with_init, with_out):
+    """The one-pass form: pieces scanned once (piece 0 from the initial state,
+    the rest from zero), outputs corrected by exp(L_t) C_t S_p^T, final state
+    composed.  Checked against the oracle and against the rescan form."""
+    dk, dv, hq, hv, online = case
+    layer = I.Layer(I.SSD, hq, hv, dk, dv, 64, "bf16", "f32")
+    law = I.GateLaw(dt_mu=-3.0, dt_bias=-1.0, a_lo=1.0, a_hi=4.0)
+    w = I.build_workload("sp", layer, [[] for _ in online], list(online), law, 7)
+    G = gpu_io.GpuWorkload(w, with_cached=False)
+    rng = np.random.default_rng(3)
+    S0_np = (0.5 * rng.standard_normal(tuple(G.S_final.shape))).astype(np.float32) if with_init else None
+    S0 = torch.from_numpy(S0_np).cuda() if with_init else None
+    o_ref, S_ref = R.scan(w, S0_np)
+    G.out.fill_(7.0)
+    ws = torch.empty(lkv.chunk_scan_sp_workspace(G.layer, w.n_req, pieces), dtype=torch.uint8, device="cuda")
+    lkv.chunk_scan_sp(G.layer, G.online.struct, 1.0, S0, G.out if with_out else None, G.S_final, pieces, ws)
+    torch.cuda.synchronize()
+    assert rel_slices(G.S_final.cpu().numpy(), S_ref) < 1e-4
+    if with_out:
+        assert max_abs(G.out.float().cpu().numpy(), o_ref) < 2e-2
+        out = G.out.clone()
+        os.environ["LKV_SSD_SP_CORRECT"] = "0"
+        try:
+            G.scan(S0, pieces=pieces)
+        finally:
+            os.environ.pop("LKV_SSD_SP_CORRECT", None)
+        torch.cuda.synchronize()
+        assert (out.float() - G.out.float()).abs().max().item() < 2e-2
+    else:
+        assert bool((G.out == 7.0).all())  # no outputs written
