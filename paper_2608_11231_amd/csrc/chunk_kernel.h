@@ -693,11 +693,16 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
         // as zero by the hardware range check, so the loads need no branches
         // and the per-lane offsets are the same for every chunk.
         const uint32_t gbytes = (FAM == FAM_GDN && p.gate_bf16) ? 2u : 4u;
-        auto prefetch = [&](int ci) {
+        // Gated DeltaNet: the stagers' own work on a chunk (its L blocks and
+        // diagonal blocks) reads only k and the gates, so q and v are committed
+        // in the other half of the chunk, next to that work: the half before it
+        // (commit, prefetch) is otherwise longer than the state waves' phase I.
+        // Mamba-2 builds its output blocks from q there, so it commits q first.
+        constexpr bool QV_LATE = FAM == FAM_GDN;
+        auto prefetch_qv = [&](int ci) {
             const int64_t c0 = t0 + (int64_t)ci * CH;
             const uint32_t n = (uint32_t)((t1 - c0) < CH ? (t1 - c0) : CH);
             const int64_t qk_off = (c0 * p.h_qk + hq) * (int64_t)DK * ES;
-            pk.load_buf(make_rsrc(reinterpret_cast<const char*>(p.k) + qk_off, n * qk_rb), 0u, qk_rb, tid_a);
             if (with_out)
                 pq.load_buf(make_rsrc(reinterpret_cast<const char*>(p.q) + qk_off, n * qk_rb), 0u, qk_rb, tid_a);
             if (load_v)
@@ -705,6 +710,18 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                                           ((c0 * p.h_v + h) * (int64_t)p.dv + row0) * ES,
                                       n * v_rb),
                             0u, v_rb, tid_a);
+        };
+        auto commit_qv = [&](int ci) {
+            const int b = ci & 1;
+            if (with_out) pq.commit(sQ(b), SK, KPL, tid_a);
+            if (load_v) pv.commit(sV(b), SV, VPL, tid_a);
+        };
+        auto prefetch = [&](int ci) {
+            const int64_t c0 = t0 + (int64_t)ci * CH;
+            const uint32_t n = (uint32_t)((t1 - c0) < CH ? (t1 - c0) : CH);
+            const int64_t qk_off = (c0 * p.h_qk + hq) * (int64_t)DK * ES;
+            pk.load_buf(make_rsrc(reinterpret_cast<const char*>(p.k) + qk_off, n * qk_rb), 0u, qk_rb, tid_a);
+            if (!QV_LATE) prefetch_qv(ci);
             // gates: lane t < CH of every stager takes token t of the chunk (raw
             // bits, widened at commit; each stager forms the gate prefix itself)
             const int64_t g_off = (c0 * p.h_v + h) * (int64_t)gbytes;
@@ -727,8 +744,7 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
         auto commit = [&](int ci) {
             const int b = ci & 1;
             pk.commit(sK(b), SK, KPL, tid_a);
-            if (with_out) pq.commit(sQ(b), SK, KPL, tid_a);
-            if (load_v) pv.commit(sV(b), SV, VPL, tid_a);
+            if (!QV_LATE) commit_qv(ci);
             if (tid_a < CH) {
                 float* G = sG(b);
                 const bool b16 = FAM == FAM_GDN && p.gate_bf16;
@@ -973,20 +989,26 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
         // prologue: chunk 0 staged and its blocks built; chunk 1 in flight.  While
         // the B-waves run chunk c, the stagers commit chunk c+1 (loaded during
         // chunk c-1), issue the loads of chunk c+2, and mask chunk c+1's diagonal
-        // blocks and build its L blocks (Mamba-2: its P blocks); the solver forms
+        // blocks and build its L blocks (Mamba-2: its P blocks), Gated DeltaNet
+        // committing q and v of chunk c+1 after those blocks; the solver forms
         // chunk c's T blocks, then inverts chunk c+1's diagonal blocks.
         // The stagers and the solver also run separate loops (same barrier
         // sequence), so the solver's registers do not overlap the prefetch ones.
         if (stager) {
             if (nch > 0) {
                 prefetch(0);
+                if (QV_LATE) prefetch_qv(0);
                 commit(0);
+                if (QV_LATE) commit_qv(0);
                 gate_rows(0);
             }
             chunk_barrier();
             if (nch > 0) {
                 a_work(0);
-                if (nch > 1) prefetch(1);
+                if (nch > 1) {
+                    prefetch(1);
+                    if (QV_LATE) prefetch_qv(1);
+                }
             }
             for (int ci = 0; ci < nch; ++ci) {
                 chunk_barrier();
@@ -996,7 +1018,13 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                 }
                 if (ci + 2 < nch) prefetch(ci + 2);  // a whole chunk of lead time
                 chunk_barrier();
-                if (ci + 1 < nch) a_work(ci + 1);
+                if (ci + 1 < nch) {
+                    a_work(ci + 1);
+                    // q / v of chunk ci+1: first read after the next barrier; their
+                    // buffer was last read in chunk ci-1
+                    if (QV_LATE) commit_qv(ci + 1);
+                }
+                if (QV_LATE && ci + 2 < nch) prefetch_qv(ci + 2);
             }
         } else {
             chunk_barrier();
