@@ -13,8 +13,8 @@ struct ComposeArgs {
     float* S;              // [n_req,h_v,dv,dk]
     float* S_steps;        // or null: the state after each block but a request's last,
                            // request r's block at position j going to row j - r
-    int32_t tiles;         // row tiles of 16*nw rows over dv
-    int32_t nw;
+    int32_t tiles;         // row tiles over dv: 16*nw rows each, 64 for nw = 8
+    int32_t nw;            // waves per workgroup: 1, 2, 4 (one 16-row tile each) or 8 (see the kernel)
     int32_t n_units;
     bool bf16_pool;
 };

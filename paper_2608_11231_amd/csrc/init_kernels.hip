@@ -188,17 +188,31 @@ hipError_t launch_compose_ssd(int32_t n_req, int32_t n_blk, int32_t H, int64_t p
 // footprint (74 KB at dk = 128) lets two workgroups share a CU.  With S_steps,
 // the state after each block but the request's last is also stored (request
 // r's position j at row j - r).
+//
+// NW = 8 splits the state's dk tiles between two waves per row tile (wave w:
+// row tile w % 4, dk half w / 4), each forming its half of S_new^T from half
+// of M^T; the halves go through LDS (bf16 hi / lo, in each lane's acc-tile
+// order) once per step, since every product needs the whole state.  A wave
+// issues about one LDS read per 30 cycles whatever its width, and with four
+// waves each reading all of M^T per step that issue time is the step's; the
+// split halves the M^T reads per wave for 16 state reads more.
 template <int DK>
 struct ComposeLds {
     static constexpr int SM = DK >= 32 ? DK + 16 : DK + 8;
     static constexpr size_t PLANE = size_t(DK) * SM;  // elements
     static __host__ __device__ constexpr size_t bytes() { return 2 * PLANE * 2; }
+    // the state halves of the eight-wave form: [4 row tiles][DK/16 tiles][hi, lo][64 lanes] x 4 bf16
+    static __host__ __device__ constexpr size_t xbytes() { return size_t(4) * (DK / 16) * 2 * 64 * 8; }
 };
 
 template <int DK, int NW, bool BF>
 __global__ __launch_bounds__(64 * NW) void compose_gdn_kernel(ComposeArgs p) {
     using Ly = ComposeLds<DK>;
     constexpr int NTK = DK / 16, SM = Ly::SM;
+    constexpr bool CS = NW == 8;              // dk halves of the state on two waves per row tile
+    static_assert(!CS || NTK % 2 == 0, "the eight-wave form needs dk >= 32");
+    constexpr int NWR = CS ? 4 : NW;          // row tiles per workgroup
+    constexpr int NOWN = CS ? NTK / 2 : NTK;  // dk tiles of the state a wave owns
     constexpr int NTH = 64 * NW;
     constexpr int NV = DK * DK / 4;              // float4 vectors of one M
     constexpr int PER = (NV + NTH - 1) / NTH;    // of them per thread
@@ -208,13 +222,19 @@ __global__ __launch_bounds__(64 * NW) void compose_gdn_kernel(ComposeArgs p) {
     // many split products per wave as it has state products, and that wave's
     // matrix-core time becomes the step's
     constexpr bool MM_SPLIT = NV % NTH == 0 && NTK % 2 == 0;
-    constexpr bool MM_SPLIT_M = MM_SPLIT && NW == 4;
+    constexpr bool MM_SPLIT_M = MM_SPLIT && NW >= 4;
     extern __shared__ __align__(16) char smem[];
     bf16* sMh = reinterpret_cast<bf16*>(smem);
     bf16* sMl = sMh + Ly::PLANE;
     const int tid = threadIdx.x;
-    const int w = tid >> 6, lane = tid & 63, g = lane >> 4, c16 = lane & 15;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, g = lane >> 4, c16 = lane & 15;
+    const int rt = CS ? (w & 3) : w;        // row tile
+    const int nt0 = CS ? (w >> 2) * NOWN : 0;  // first dk tile of the state this wave owns
     const bf16x8 negI = neg_eye(g, c16);
+    // the state halves (eight-wave form): slot of dk tile nt, plane pl of this row tile
+    auto sx = [&](int nt, int pl) {
+        return reinterpret_cast<bf16x4*>(smem + Ly::bytes()) + ((rt * NTK + nt) * 2 + pl) * 64 + lane;
+    };
     // units: the row tiles of one (request, head) adjacent, then the request
     // index fastest, so each XCD's range holds a few heads of every request
     // (ragged block counts load the XCDs evenly)
@@ -223,7 +243,7 @@ __global__ __launch_bounds__(64 * NW) void compose_gdn_kernel(ComposeArgs p) {
     const int tile = u % p.tiles;
     const int r = (u / p.tiles) % n_req;
     const int h = u / (p.tiles * n_req);
-    const int my_row = tile * 16 * NW + 16 * w + c16;
+    const int my_row = tile * 16 * NWR + 16 * rt + c16;
 
     int32_t b0 = p.blk_cu[r], b1 = p.blk_cu[r + 1];
     b0 = b0 < 0 ? 0 : (b0 > p.n_ids ? p.n_ids : b0);
@@ -231,9 +251,9 @@ __global__ __launch_bounds__(64 * NW) void compose_gdn_kernel(ComposeArgs p) {
 
     auto valid = [&](int32_t id) { return id >= 0 && id < p.n_blk; };
     auto b_rows = [&](int32_t id) {  // element offset of this lane's B row segment
-        return (((int64_t)id * p.h_v + h) * p.dv + my_row) * DK + 4 * g;
+        return (((int64_t)id * p.h_v + h) * p.dv + my_row) * DK + 16 * nt0 + 4 * g;
     };
-    f32x4 mreg[PER], breg[NTK];
+    f32x4 mreg[PER], breg[NOWN];
     auto load_m = [&](int32_t id) {
         // plain loads: the head's other row tiles read the same M through the XCD's L2
         const f32x4* Mj = reinterpret_cast<const f32x4*>(p.M_pool + ((int64_t)id * p.h_v + h) * DK * DK);
@@ -246,7 +266,7 @@ __global__ __launch_bounds__(64 * NW) void compose_gdn_kernel(ComposeArgs p) {
     auto load_b = [&](int32_t id) {
         const int64_t Bj = b_rows(id);
 #pragma unroll
-        for (int nt = 0; nt < NTK; ++nt) breg[nt] = pool4<BF>(p.B_pool, Bj + 16 * nt);
+        for (int nt = 0; nt < NOWN; ++nt) breg[nt] = pool4<BF>(p.B_pool, Bj + 16 * nt);
     };
     // M (in mreg) -> bf16 hi / lo planes in LDS, row-major
     auto stage_m = [&]() {
@@ -268,9 +288,9 @@ __global__ __launch_bounds__(64 * NW) void compose_gdn_kernel(ComposeArgs p) {
     typedef __attribute__((address_space(4))) const int32_t const_i32;
     const const_i32* ids_c = (const const_i32*)p.blk_ids;
     auto id_at = [&](int32_t j) { return ids_c[j]; };
-    f32x4 S[NTK];
+    f32x4 S[NOWN];
 #pragma unroll
-    for (int nt = 0; nt < NTK; ++nt) S[nt] = zero4();
+    for (int nt = 0; nt < NOWN; ++nt) S[nt] = zero4();
     // block ids are the same for every wave of the workgroup, so every branch
     // on them below is uniform; bad_at is the first position with an invalid id
     int32_t bad_at = b1;
@@ -297,21 +317,30 @@ __global__ __launch_bounds__(64 * NW) void compose_gdn_kernel(ComposeArgs p) {
     }
     for (int32_t j = b0; j < b1 && j < bad_at; ++j) {
         if (j + 2 < b1) id2 = id_checked(j + 2);
-        lds_barrier();  // M_j staged by every wave
-        f32x4 acc[NTK];
+        lds_barrier();  // M_j staged by every wave (eight waves: and the state halves published)
+        f32x4 acc[NOWN];
 #pragma unroll
-        for (int nt = 0; nt < NTK; ++nt) acc[nt] = breg[nt];
+        for (int nt = 0; nt < NOWN; ++nt) acc[nt] = breg[nt];
         load_b(j + 1 < bad_at ? id1 : id0);
         // B_{j+1} stays ahead of M_{j+2} in issue order: the memory counter is
         // in order, so waiting for one waits for everything issued before it
         __builtin_amdgcn_sched_barrier(0);
         if (j > b0) {
             bf16x4 Sh[NTK], Sl[NTK];
+            if constexpr (CS) {
+                // the whole state, both halves as published after the previous step
 #pragma unroll
-            for (int nt = 0; nt < NTK; ++nt) {
-                const Split4 sp = MM_SPLIT ? split4_mm(S[nt], negI) : split4(S[nt]);
-                Sh[nt] = sp.hi;
-                Sl[nt] = sp.lo;
+                for (int nt = 0; nt < NTK; ++nt) {
+                    Sh[nt] = *sx(nt, 0);
+                    Sl[nt] = *sx(nt, 1);
+                }
+            } else {
+#pragma unroll
+                for (int nt = 0; nt < NTK; ++nt) {
+                    const Split4 sp = MM_SPLIT ? split4_mm(S[nt], negI) : split4(S[nt]);
+                    Sh[nt] = sp.hi;
+                    Sl[nt] = sp.lo;
+                }
             }
             // S_new^T tile nt (rows 16nt..16nt+15) = M^T S^T + B^T: A fragments of
             // M^T come straight from the row-major planes through transposed LDS
@@ -326,16 +355,16 @@ __global__ __launch_bounds__(64 * NW) void compose_gdn_kernel(ComposeArgs p) {
             } else {
 #pragma unroll
                 for (int kg = 0; kg < NTK; kg += 2) {
-                    bf16x4 a0[NTK], a1[NTK], c0[NTK], c1[NTK];
+                    bf16x4 a0[NOWN], a1[NOWN], c0[NOWN], c1[NOWN];
 #pragma unroll
-                    for (int nt = 0; nt < NTK; ++nt) {
-                        a0[nt] = lds4_tr(sMh, SM, 16 * kg, 16 * nt, g, c16);
-                        a1[nt] = lds4_tr(sMh, SM, 16 * kg + 16, 16 * nt, g, c16);
-                        c0[nt] = lds4_tr(sMl, SM, 16 * kg, 16 * nt, g, c16);
-                        c1[nt] = lds4_tr(sMl, SM, 16 * kg + 16, 16 * nt, g, c16);
+                    for (int nt = 0; nt < NOWN; ++nt) {
+                        a0[nt] = lds4_tr(sMh, SM, 16 * kg, 16 * (nt0 + nt), g, c16);
+                        a1[nt] = lds4_tr(sMh, SM, 16 * kg + 16, 16 * (nt0 + nt), g, c16);
+                        c0[nt] = lds4_tr(sMl, SM, 16 * kg, 16 * (nt0 + nt), g, c16);
+                        c1[nt] = lds4_tr(sMl, SM, 16 * kg + 16, 16 * (nt0 + nt), g, c16);
                     }
 #pragma unroll
-                    for (int nt = 0; nt < NTK; ++nt) {
+                    for (int nt = 0; nt < NOWN; ++nt) {
                         acc[nt] = mma32(a0[nt], a1[nt], Sh[kg], Sh[kg + 1], acc[nt]);
                         acc[nt] = mma32(a0[nt], a1[nt], Sl[kg], Sl[kg + 1], acc[nt]);
                         acc[nt] = mma32(c0[nt], c1[nt], Sh[kg], Sh[kg + 1], acc[nt]);
@@ -344,16 +373,25 @@ __global__ __launch_bounds__(64 * NW) void compose_gdn_kernel(ComposeArgs p) {
             }
         }
         // stage M_{j+1} (requested one step ago) and request M_{j+2}
-        lds_barrier();  // every wave is done reading M_j
+        lds_barrier();  // every wave is done reading M_j (and the state halves)
         stage_m();
         load_m(j + 2 < bad_at ? id2 : id1);
 #pragma unroll
-        for (int nt = 0; nt < NTK; ++nt) S[nt] = acc[nt];
+        for (int nt = 0; nt < NOWN; ++nt) S[nt] = acc[nt];
+        if constexpr (CS) {
+            // this wave's half of the new state, split, for every wave of its row tile
+#pragma unroll
+            for (int nt = 0; nt < NOWN; ++nt) {
+                const Split4 sp = split4_mm(acc[nt], negI);
+                *sx(nt0 + nt, 0) = sp.hi;
+                *sx(nt0 + nt, 1) = sp.lo;
+            }
+        }
         if (p.S_steps && j + 1 < b1) {
             // the state after this block (position j), a start state for a later step
-            float* dst = p.S_steps + ((((int64_t)j - r) * p.h_v + h) * p.dv + my_row) * DK + 4 * g;
+            float* dst = p.S_steps + ((((int64_t)j - r) * p.h_v + h) * p.dv + my_row) * DK + 16 * nt0 + 4 * g;
 #pragma unroll
-            for (int nt = 0; nt < NTK; ++nt) *reinterpret_cast<f32x4*>(dst + 16 * nt) = acc[nt];
+            for (int nt = 0; nt < NOWN; ++nt) *reinterpret_cast<f32x4*>(dst + 16 * nt) = acc[nt];
         }
         id0 = id1;
         id1 = id2;
@@ -361,16 +399,16 @@ __global__ __launch_bounds__(64 * NW) void compose_gdn_kernel(ComposeArgs p) {
     if (bad_at < b1) {
         const float f = __builtin_nanf("");
 #pragma unroll
-        for (int nt = 0; nt < NTK; ++nt) S[nt] = f32x4{f, f, f, f};
+        for (int nt = 0; nt < NOWN; ++nt) S[nt] = f32x4{f, f, f, f};
     }
-    float* dst = p.S + (((int64_t)r * p.h_v + h) * p.dv + my_row) * DK + 4 * g;
+    float* dst = p.S + (((int64_t)r * p.h_v + h) * p.dv + my_row) * DK + 16 * nt0 + 4 * g;
 #pragma unroll
-    for (int nt = 0; nt < NTK; ++nt) *reinterpret_cast<f32x4*>(dst + 16 * nt) = S[nt];
+    for (int nt = 0; nt < NOWN; ++nt) *reinterpret_cast<f32x4*>(dst + 16 * nt) = S[nt];
 }
 
 template <int DK, int NW>
 static hipError_t launch_compose_gdn_nw(const ComposeArgs& a, hipStream_t st) {
-    const size_t lds = ComposeLds<DK>::bytes();
+    const size_t lds = ComposeLds<DK>::bytes() + (NW == 8 ? ComposeLds<DK>::xbytes() : 0);
     auto kern = a.bf16_pool ? compose_gdn_kernel<DK, NW, true> : compose_gdn_kernel<DK, NW, false>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -385,6 +423,9 @@ static hipError_t launch_compose_gdn_t(const ComposeArgs& a, hipStream_t st) {
         case 1: return launch_compose_gdn_nw<DK, 1>(a, st);
         case 2: return launch_compose_gdn_nw<DK, 2>(a, st);
         case 4: return launch_compose_gdn_nw<DK, 4>(a, st);
+        case 8:
+            if constexpr (DK >= 32) return launch_compose_gdn_nw<DK, 8>(a, st);
+            return hipErrorInvalidValue;
     }
     return hipErrorInvalidValue;
 }

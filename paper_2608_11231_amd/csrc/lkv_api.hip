@@ -233,13 +233,17 @@ lkv_status init_compose(const lkv_layer* L, int32_t n_req, int32_t n_blk, const 
                                              blk_cu, n_ids, S_init, S_steps, st));
     }
     const int64_t pairs = (int64_t)n_req * L->h_v;
-    // state-row waves per workgroup: four (64 rows) wherever dv allows.  Each
-    // step stages the whole M in LDS; four waves share that staging, and the
-    // step's latency -- not the number of workgroups -- sets the time (at 8K,
-    // 64 four-wave workgroups compose faster than 256 one-wave ones)
+    // waves per workgroup: eight on 64 state rows (two per row tile, each
+    // with half of the state's dk tiles) where dk >= 32 and dv allows, else
+    // four, two or one of 16 rows each.  Each step stages the whole M in LDS;
+    // the waves share that staging, and the step's latency -- not the number
+    // of workgroups -- sets the time (at 8K, 64 four-wave workgroups compose
+    // faster than 256 one-wave ones)
     int nw = env_int("LKV_COMPOSE_NW", 0);
-    if (nw != 1 && nw != 2 && nw != 4) nw = 4;
-    while (nw > 1 && L->dv % (16 * nw)) nw >>= 1;
+    if (nw != 1 && nw != 2 && nw != 4 && nw != 8) nw = 8;
+    if (nw == 8 && (L->dk < 32 || L->dv % 64)) nw = 4;
+    while (nw > 1 && nw != 8 && L->dv % (16 * nw)) nw >>= 1;
+    const int rows = nw == 8 ? 64 : 16 * nw;  // state rows per workgroup
     ComposeArgs a = {};
     a.B_pool = B_pool;
     a.bf16_pool = bf16_pool;
@@ -253,7 +257,7 @@ lkv_status init_compose(const lkv_layer* L, int32_t n_req, int32_t n_blk, const 
     a.S = S_init;
     a.S_steps = S_steps;
     a.nw = nw;
-    a.tiles = L->dv / (16 * nw);
+    a.tiles = L->dv / rows;
     const int64_t units = pairs * a.tiles;
     if (units >= (INT64_C(1) << 31)) return LKV_E_SHAPE;
     a.n_units = (int32_t)units;
