@@ -321,6 +321,7 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
         // acc layout: S[rt][nt] holds S[row][16nt + 4g + r]
         auto row_of = [&](int rt) { return row0 + 16 * (RT * w + rt) + c16; };
         const bf16x8 negI = neg_eye(g, c16);  // hi / lo splits on the matrix core
+        const bf16x8 negIh = neg_eye_hi(g, c16);
         f32x4 S[RT][NTK];
         // initial state row: segment s's own (S_init) or, with src, a pool row
         // (LinearKV's single cached state read straight from the cache pool)
@@ -358,16 +359,29 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
         bf16x4 Sh[RT][NTK], Sl[RT][NTK];
         auto split_state = [&]() {
 #pragma unroll
-            for (int rt = 0; rt < RT; ++rt)
+            for (int rt = 0; rt < RT; ++rt) {
+                // 64-token chunks: S comes from a 32-wide MFMA chain, which the
+                // 32-wide split product may follow (dk tiles in pairs, as K S^T
+                // reads them); 16-token chunks update S 16-wide, and one chain
+                // never mixes the two shapes
+                if constexpr (NTC == 4 && NTK % 2 == 0) {
 #pragma unroll
-                for (int nt = 0; nt < NTK; ++nt) {
-                    // 64-token chunks: S comes from a 32-wide MFMA chain, which the
-                    // 32-wide split product may follow; 16-token chunks update S
-                    // 16-wide, and one chain never mixes the two shapes
-                    const Split4 sp = NTC == 4 ? split4_mm(S[rt][nt], negI) : split4(S[rt][nt]);
-                    Sh[rt][nt] = sp.hi;
-                    Sl[rt][nt] = sp.lo;
+                    for (int nt = 0; nt < NTK; nt += 2) {
+                        const Split8 sp = split8_mm(S[rt][nt], S[rt][nt + 1], negI, negIh);
+                        Sh[rt][nt] = sp.hi0;
+                        Sh[rt][nt + 1] = sp.hi1;
+                        Sl[rt][nt] = sp.lo0;
+                        Sl[rt][nt + 1] = sp.lo1;
+                    }
+                } else {
+#pragma unroll
+                    for (int nt = 0; nt < NTK; ++nt) {
+                        const Split4 sp = NTC == 4 ? split4_mm(S[rt][nt], negI) : split4(S[rt][nt]);
+                        Sh[rt][nt] = sp.hi;
+                        Sl[rt][nt] = sp.lo;
+                    }
                 }
+            }
         };
         split_state();
         chunk_barrier();  // prologue: chunk 0 staged by the A-waves
@@ -523,6 +537,16 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                         Uh[rt][mt] = us.hi;
                         Ul[rt][mt] = us.lo;
                     };
+                    // token tiles mt, mt + 1 together (the 32-wide slice later products read)
+                    auto split_u2 = [&](int rt, int mt, f32x4 v0, f32x4 v1) {
+                        U[rt][mt] = v0;
+                        U[rt][mt + 1] = v1;
+                        const Split8 us = split8_mm(v0, v1, negI, negIh);
+                        Uh[rt][mt] = us.hi0;
+                        Uh[rt][mt + 1] = us.hi1;
+                        Ul[rt][mt] = us.lo0;
+                        Ul[rt][mt + 1] = us.lo1;
+                    };
                     if constexpr (NTC == 1) {
 #pragma unroll
                         for (int rt = 0; rt < RT; ++rt) {
@@ -549,18 +573,17 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                         // stage 1: U_0 = N_0 X_0, U_1 = T_10 X_0 + N_1 X_1
 #pragma unroll
                         for (int rt = 0; rt < RT; ++rt) {
-                            const Split4 x0 = split4_mm(X[rt][0], negI), x1 = split4_mm(X[rt][1], negI);
-                            const f32x4 u0h = mma16(Nh[0], x0.hi, zero4());
-                            const f32x4 u1h = mma32(t10h, Nh[1], x0.hi, x1.hi, zero4());
-                            f32x4 u0l = mma16(Nh[0], x0.lo, zero4());
-                            f32x4 u1l = mma32(t10h, Nh[1], x0.lo, x1.lo, zero4());
-                            u0l = mma16(Nl[0], x0.hi, u0l);
-                            u1l = mma32(t10l, Nl[1], x0.hi, x1.hi, u1l);
-                            split_u(rt, 0, u0h + u0l);
-                            split_u(rt, 1, u1h + u1l);
+                            const Split8 x01 = split8_mm(X[rt][0], X[rt][1], negI, negIh);
+                            const f32x4 u0h = mma16(Nh[0], x01.hi0, zero4());
+                            const f32x4 u1h = mma32(t10h, Nh[1], x01.hi0, x01.hi1, zero4());
+                            f32x4 u0l = mma16(Nh[0], x01.lo0, zero4());
+                            f32x4 u1l = mma32(t10h, Nh[1], x01.lo0, x01.lo1, zero4());
+                            u0l = mma16(Nl[0], x01.hi0, u0l);
+                            u1l = mma32(t10l, Nl[1], x01.hi0, x01.hi1, u1l);
+                            split_u2(rt, 0, u0h + u0l, u1h + u1l);
                         }
                         // stage 2: R_2 = X_2 - L_20 U_0 - L_21 U_1, R_3 = X_3 - L_30 U_0 - L_31 U_1
-                        Split4 x2[RT], x3[RT];
+                        Split8 x23[RT];
 #pragma unroll
                         for (int rt = 0; rt < RT; ++rt) {
                             const f32x4 r2h = mma32(Lh[0], Lh[1], Uh[rt][0], Uh[rt][1], X[rt][2]);
@@ -569,20 +592,18 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                             f32x4 r3l = mma32(Lh[2], Lh[3], Ul[rt][0], Ul[rt][1], zero4());
                             r2l = mma32(Ll[0], Ll[1], Uh[rt][0], Uh[rt][1], r2l);
                             r3l = mma32(Ll[2], Ll[3], Uh[rt][0], Uh[rt][1], r3l);
-                            x2[rt] = split4_mm(r2h + r2l, negI);
-                            x3[rt] = split4_mm(r3h + r3l, negI);
+                            x23[rt] = split8_mm(r2h + r2l, r3h + r3l, negI, negIh);
                         }
                         // stage 3: U_2 = N_2 R_2, U_3 = T_32 R_2 + N_3 R_3
 #pragma unroll
                         for (int rt = 0; rt < RT; ++rt) {
-                            const f32x4 u2h = mma16(Nh[2], x2[rt].hi, zero4());
-                            const f32x4 u3h = mma32(t32h, Nh[3], x2[rt].hi, x3[rt].hi, zero4());
-                            f32x4 u2l = mma16(Nh[2], x2[rt].lo, zero4());
-                            f32x4 u3l = mma32(t32h, Nh[3], x2[rt].lo, x3[rt].lo, zero4());
-                            u2l = mma16(Nl[2], x2[rt].hi, u2l);
-                            u3l = mma32(t32l, Nl[3], x2[rt].hi, x3[rt].hi, u3l);
-                            split_u(rt, 2, u2h + u2l);
-                            split_u(rt, 3, u3h + u3l);
+                            const f32x4 u2h = mma16(Nh[2], x23[rt].hi0, zero4());
+                            const f32x4 u3h = mma32(t32h, Nh[3], x23[rt].hi0, x23[rt].hi1, zero4());
+                            f32x4 u2l = mma16(Nh[2], x23[rt].lo0, zero4());
+                            f32x4 u3l = mma32(t32h, Nh[3], x23[rt].lo0, x23[rt].lo1, zero4());
+                            u2l = mma16(Nl[2], x23[rt].hi0, u2l);
+                            u3l = mma32(t32l, Nl[3], x23[rt].hi0, x23[rt].hi1, u3l);
+                            split_u2(rt, 2, u2h + u2l, u3h + u3l);
                         }
                     }
                 } else {
@@ -644,14 +665,30 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                 }
                 // S <- b_C S + K^T diag(w) U   (all dk tiles and row tiles interleaved)
                 bf16x4 Wh[RT][NTC], Wl[RT][NTC];
+                if constexpr (NTC == 4) {
 #pragma unroll
-                for (int mt = 0; mt < NTC; ++mt) {
-                    const f32x4 wt = lds4f(G + 3 * CH + 16 * mt + 4 * g);
+                    for (int mt = 0; mt < NTC; mt += 2) {
+                        const f32x4 w0 = lds4f(G + 3 * CH + 16 * mt + 4 * g);
+                        const f32x4 w1 = lds4f(G + 3 * CH + 16 * mt + 16 + 4 * g);
 #pragma unroll
-                    for (int rt = 0; rt < RT; ++rt) {
-                        const Split4 sp = split4_mm(wt * U[rt][mt], negI);
-                        Wh[rt][mt] = sp.hi;
-                        Wl[rt][mt] = sp.lo;
+                        for (int rt = 0; rt < RT; ++rt) {
+                            const Split8 sp = split8_mm(w0 * U[rt][mt], w1 * U[rt][mt + 1], negI, negIh);
+                            Wh[rt][mt] = sp.hi0;
+                            Wh[rt][mt + 1] = sp.hi1;
+                            Wl[rt][mt] = sp.lo0;
+                            Wl[rt][mt + 1] = sp.lo1;
+                        }
+                    }
+                } else {
+#pragma unroll
+                    for (int mt = 0; mt < NTC; ++mt) {
+                        const f32x4 wt = lds4f(G + 3 * CH + 16 * mt + 4 * g);
+#pragma unroll
+                        for (int rt = 0; rt < RT; ++rt) {
+                            const Split4 sp = split4_mm(wt * U[rt][mt], negI);
+                            Wh[rt][mt] = sp.hi;
+                            Wl[rt][mt] = sp.lo;
+                        }
                     }
                 }
                 const float bC = G[5 * CH];

@@ -109,6 +109,33 @@ __device__ __forceinline__ Split4 split4_mm(f32x4 x, bf16x8 negI) {
     return s;
 }
 
+// Two acc tiles split at once, for the common case where their parts feed a
+// 32-wide product as its two 16-slices.  Both tiles' hi parts form one 8-element
+// B operand, which is exactly that product's fragment; the first tile's x - hi
+// takes the negated identity on the first 16-slice (neg_eye), the second's the
+// same identity moved to the second slice (neg_eye_hi).  No operand needs zero
+// padding or reassembly, and every value is bit-identical to split4.
+__device__ __forceinline__ bf16x8 neg_eye_hi(int g, int c) {
+    bf16x8 e;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) e[j] = (j >= 4 && 4 * g + j - 4 == c) ? (bf16)-1.f : (bf16)0.f;
+    return e;
+}
+struct Split8 {
+    bf16x4 hi0, hi1, lo0, lo1;
+};
+__device__ __forceinline__ Split8 split8_mm(f32x4 x0, f32x4 x1, bf16x8 negI, bf16x8 negIh) {
+    const bf16x8 hi = __builtin_shufflevector(to_bf16(x0), to_bf16(x1), 0, 1, 2, 3, 4, 5, 6, 7);
+    const bf16x4 l0 = to_bf16(__builtin_amdgcn_mfma_f32_16x16x32_bf16(negI, hi, x0, 0, 0, 0));
+    const bf16x4 l1 = to_bf16(__builtin_amdgcn_mfma_f32_16x16x32_bf16(negIh, hi, x1, 0, 0, 0));
+    Split8 s;
+    s.hi0 = __builtin_shufflevector(hi, hi, 0, 1, 2, 3);
+    s.hi1 = __builtin_shufflevector(hi, hi, 4, 5, 6, 7);
+    s.lo0 = l0;
+    s.lo1 = l1;
+    return s;
+}
+
 // LDS loads of 4 / 8 consecutive elements (8 / 16 / 16 bytes)
 __device__ __forceinline__ bf16x4 lds4(const bf16* p) { return *reinterpret_cast<const bf16x4*>(p); }
 __device__ __forceinline__ bf16x8 lds8(const bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
