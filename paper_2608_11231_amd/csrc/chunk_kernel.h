@@ -55,6 +55,9 @@ namespace lkv {
 
 enum { FAM_GDN = 0, FAM_SSD = 1 };
 constexpr int NA = 4;  // A-waves per workgroup
+// The state waves keep S / e^lam with lam >= -LAM_FLOOR (see gate_rows): the
+// stored state stays within e^32 (about 8e13) of the true one, far from fp32's range.
+constexpr float LAM_FLOOR = 32.f;
 
 struct ScanArgs {
     const int32_t* cu;
@@ -521,7 +524,8 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                     // with T_A = [[N_0, 0], [T_10, N_1]], T_B = [[N_2, 0], [T_32, N_3]] (the
                     // 16x16 diagonal inverses N and T_10 = -N_1 L_10 N_0, T_32 = -N_3 L_32 N_2
                     // come from the A-waves).  Three dependent stages, the row tiles
-                    // interleaved; the hi*hi and the correction passes accumulate apart.
+                    // interleaved; each product's three passes chain on one accumulator
+                    // (the row tiles and output tiles of a stage keep RT * 2 chains in flight).
                     // All fragments are requested before the first product.
                     const bf16* LT = sLT(b);
                     const bf16* NT = sNT(b);
@@ -574,36 +578,36 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
 #pragma unroll
                         for (int rt = 0; rt < RT; ++rt) {
                             const Split8 x01 = split8_mm(X[rt][0], X[rt][1], negI, negIh);
-                            const f32x4 u0h = mma16(Nh[0], x01.hi0, zero4());
-                            const f32x4 u1h = mma32(t10h, Nh[1], x01.hi0, x01.hi1, zero4());
-                            f32x4 u0l = mma16(Nh[0], x01.lo0, zero4());
-                            f32x4 u1l = mma32(t10h, Nh[1], x01.lo0, x01.lo1, zero4());
-                            u0l = mma16(Nl[0], x01.hi0, u0l);
-                            u1l = mma32(t10l, Nl[1], x01.hi0, x01.hi1, u1l);
-                            split_u2(rt, 0, u0h + u0l, u1h + u1l);
+                            f32x4 u0 = mma16(Nh[0], x01.hi0, zero4());
+                            f32x4 u1 = mma32(t10h, Nh[1], x01.hi0, x01.hi1, zero4());
+                            u0 = mma16(Nh[0], x01.lo0, u0);
+                            u1 = mma32(t10h, Nh[1], x01.lo0, x01.lo1, u1);
+                            u0 = mma16(Nl[0], x01.hi0, u0);
+                            u1 = mma32(t10l, Nl[1], x01.hi0, x01.hi1, u1);
+                            split_u2(rt, 0, u0, u1);
                         }
                         // stage 2: R_2 = X_2 - L_20 U_0 - L_21 U_1, R_3 = X_3 - L_30 U_0 - L_31 U_1
                         Split8 x23[RT];
 #pragma unroll
                         for (int rt = 0; rt < RT; ++rt) {
-                            const f32x4 r2h = mma32(Lh[0], Lh[1], Uh[rt][0], Uh[rt][1], X[rt][2]);
-                            const f32x4 r3h = mma32(Lh[2], Lh[3], Uh[rt][0], Uh[rt][1], X[rt][3]);
-                            f32x4 r2l = mma32(Lh[0], Lh[1], Ul[rt][0], Ul[rt][1], zero4());
-                            f32x4 r3l = mma32(Lh[2], Lh[3], Ul[rt][0], Ul[rt][1], zero4());
-                            r2l = mma32(Ll[0], Ll[1], Uh[rt][0], Uh[rt][1], r2l);
-                            r3l = mma32(Ll[2], Ll[3], Uh[rt][0], Uh[rt][1], r3l);
-                            x23[rt] = split8_mm(r2h + r2l, r3h + r3l, negI, negIh);
+                            f32x4 r2 = mma32(Lh[0], Lh[1], Uh[rt][0], Uh[rt][1], X[rt][2]);
+                            f32x4 r3 = mma32(Lh[2], Lh[3], Uh[rt][0], Uh[rt][1], X[rt][3]);
+                            r2 = mma32(Lh[0], Lh[1], Ul[rt][0], Ul[rt][1], r2);
+                            r3 = mma32(Lh[2], Lh[3], Ul[rt][0], Ul[rt][1], r3);
+                            r2 = mma32(Ll[0], Ll[1], Uh[rt][0], Uh[rt][1], r2);
+                            r3 = mma32(Ll[2], Ll[3], Uh[rt][0], Uh[rt][1], r3);
+                            x23[rt] = split8_mm(r2, r3, negI, negIh);
                         }
                         // stage 3: U_2 = N_2 R_2, U_3 = T_32 R_2 + N_3 R_3
 #pragma unroll
                         for (int rt = 0; rt < RT; ++rt) {
-                            const f32x4 u2h = mma16(Nh[2], x23[rt].hi0, zero4());
-                            const f32x4 u3h = mma32(t32h, Nh[3], x23[rt].hi0, x23[rt].hi1, zero4());
-                            f32x4 u2l = mma16(Nh[2], x23[rt].lo0, zero4());
-                            f32x4 u3l = mma32(t32h, Nh[3], x23[rt].lo0, x23[rt].lo1, zero4());
-                            u2l = mma16(Nl[2], x23[rt].hi0, u2l);
-                            u3l = mma32(t32l, Nl[3], x23[rt].hi0, x23[rt].hi1, u3l);
-                            split_u2(rt, 2, u2h + u2l, u3h + u3l);
+                            f32x4 u2 = mma16(Nh[2], x23[rt].hi0, zero4());
+                            f32x4 u3 = mma32(t32h, Nh[3], x23[rt].hi0, x23[rt].hi1, zero4());
+                            u2 = mma16(Nh[2], x23[rt].lo0, u2);
+                            u3 = mma32(t32h, Nh[3], x23[rt].lo0, x23[rt].lo1, u3);
+                            u2 = mma16(Nl[2], x23[rt].hi0, u2);
+                            u3 = mma32(t32l, Nl[3], x23[rt].hi0, x23[rt].hi1, u3);
+                            split_u2(rt, 2, u2, u3);
                         }
                     }
                 } else {
@@ -691,11 +695,16 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                         }
                     }
                 }
-                const float bC = G[5 * CH];
+                // state factor: 1 (the decay stays in the stored scale) or a rescale;
+                // compared as bits so the branch is scalar
+                const uint32_t rho = (uint32_t)__builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, G[5 * CH]));
+                if (rho != 0x3f800000u) {
+                    const float r = __builtin_bit_cast(float, rho);
 #pragma unroll
-                for (int rt = 0; rt < RT; ++rt)
+                    for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-                    for (int nt = 0; nt < NTK; ++nt) S[rt][nt] = bC * S[rt][nt];
+                        for (int nt = 0; nt < NTK; ++nt) S[rt][nt] = r * S[rt][nt];
+                }
                 if constexpr (RT == 1)
                     mgemm_tr<DK, NTK, F32IO, true>(Kb, KPL, SK, Wh[0], Wl[0], NTC, g, c16, S[0]);
                 else
@@ -705,6 +714,14 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
         }
         float* dst = mtile ? p.M_out : p.S_final;
         if (dst) {
+            // back from the stored scale (the last chunk's gate rows are still in place)
+            if (nch > 0) {
+                const float sc = sG((nch - 1) & 1)[5 * CH + 1];
+#pragma unroll
+                for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+                    for (int nt = 0; nt < NTK; ++nt) S[rt][nt] = sc * S[rt][nt];
+            }
             const int rows = mtile ? DK : p.dv;
 #pragma unroll
             for (int rt = 0; rt < RT; ++rt)
@@ -723,6 +740,7 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
         TileRegs<CH, 16 * NB * RT, F32IO, 64 * NSTG> pv;
         uint32_t pg = 0u, pb = 0u;  // gates stay raw bits until commit (no early wait on the loads)
         float lam_sum = 0.f;
+        float lam = 0.f;  // stager 0: log scale of the state waves' stored state
         constexpr int ES = F32IO ? 4 : 2;
         const uint32_t qk_rb = (uint32_t)(p.h_qk * DK * ES), v_rb = (uint32_t)(p.h_v * p.dv * ES);
         // Chunk loads go through buffer resources that end at the chunk's last
@@ -804,18 +822,33 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
             const float gtot = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, gc), CH - 1));
             gcw[lane] = gc;
             if (wa == 0) {
+                // The state waves hold S / e^lam (lam = the log decay since the last
+                // rescale), so the chunk's decay b_C needs no pass over the state:
+                // it moves into lam, and the per-token rows carry e^lam instead.
+                // Once lam would drop below -LAM_FLOOR the state is rescaled by
+                // e^lam (the state factor below) and lam restarts at 0, which keeps
+                // S / e^lam within e^LAM_FLOOR of S.  Mamba-2 rescales every chunk
+                // (lam stays 0: the plain b_C S form, which its eight-wave scan
+                // kernel reproduces bit for bit).
+                const float lam_in = lam;
+                float lam_out = lam_in + gtot, rho = 1.f;
+                if (FAM != FAM_GDN || lam_out < -LAM_FLOOR) {
+                    rho = __expf(lam_out);
+                    lam_out = 0.f;
+                }
                 if (lane < CH) {
-                    const float bt = __expf(gc);
+                    const float bt = __expf(gc + lam_in);  // b_t against the stored state
                     G[2 * CH + lane] = bt;
-                    const float wt = __expf(gtot - gc);
+                    const float wt = __expf(gtot - gc - lam_out);
                     G[3 * CH + lane] = (FAM == FAM_GDN) ? wt : graw * wt;
                     G[4 * CH + lane] = gc;
                     if (FAM == FAM_GDN) G[Ly::BB_ROW + lane] = __builtin_bit_cast(float, b16 ? pb << 16 : pb) * bt;
                 }
                 if (lane == 0) {
-                    G[5 * CH] = __expf(gtot);
-                    G[5 * CH + 1] = gtot;
+                    G[5 * CH] = rho;                    // state factor of this chunk's update
+                    G[5 * CH + 1] = __expf(lam_out);    // stored -> true state after it
                 }
+                lam = lam_out;
                 lam_sum += gtot;
             }
         };
