@@ -236,79 +236,93 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
             const bf16* Kb = sK(b);
             const bf16* Ab = KL ? sK(b) : sQ(b);
             const float* G = sG(b);
-            auto item_mt = [](int i) { return KL ? off_mt(SLOT + i * NSLOT) : low_mt(SLOT + i * NSLOT); };
-            auto item_nt = [](int i) {
-                const int j = SLOT + i * NSLOT;
-                return KL ? j - off_index(off_mt(j), 0) : j - low_index(low_mt(j), 0);
-            };
-            f32x4 acc[NMY];
-#pragma unroll
-            for (int i = 0; i < NMY; ++i) acc[i] = zero4();
-            if constexpr (NK == 1) {
-#pragma unroll
-                for (int i = 0; i < NMY; ++i) {
-                    const bf16* ar = Ab + (16 * item_mt(i) + c16) * SK + 4 * g;
-                    const bf16* br = Kb + (16 * item_nt(i) + c16) * SK + 4 * g;
-                    acc[i] = mma16(lds4(ar), lds4(br), acc[i]);
-                    if (F32IO) {
-                        acc[i] = mma16(lds4(ar), lds4(br + KPL), acc[i]);
-                        acc[i] = mma16(lds4(ar + KPL), lds4(br), acc[i]);
-                    }
-                }
-            } else {
-                // fragments of slice kp+1 are requested before the products of slice kp
-                constexpr int NKP = NK / 2, FPL = F32IO ? 2 : 1;
-                bf16x8 fa[2][FPL][NMY], fb[2][FPL][NMY];
-                auto fetch = [&](int kp, int buf) {
-#pragma unroll
-                    for (int i = 0; i < NMY; ++i) {
-                        const bf16* ar = Ab + (16 * item_mt(i) + c16) * SK + 32 * kp + 8 * g;
-                        const bf16* br = Kb + (16 * item_nt(i) + c16) * SK + 32 * kp + 8 * g;
-#pragma unroll
-                        for (int pl = 0; pl < FPL; ++pl) {
-                            fa[buf][pl][i] = lds8(ar + pl * KPL);
-                            fb[buf][pl][i] = lds8(br + pl * KPL);
-                        }
-                    }
+            // more than five blocks (one or two state waves building all of a
+            // chunk's output blocks) are built in batches of four; with fp32 io
+            // (fragments with lo planes) in batches of two, or one by one for a
+            // single state wave: one batch's fragments, double-buffered, then fit
+            // the registers with the state
+            constexpr int BAT = F32IO ? (NMY > 5 ? 1 : (NMY > 3 ? 2 : NMY)) : (NMY > 5 ? 4 : NMY);
+            constexpr int NBAT = (NMY + BAT - 1) / BAT;
+            auto batch = [&](auto bi_c) {
+                constexpr int I0 = decltype(bi_c)::value * BAT;
+                constexpr int BN = (NMY - I0) < BAT ? (NMY - I0) : BAT;
+                auto item_mt = [](int i) {
+                    return KL ? off_mt(SLOT + (I0 + i) * NSLOT) : low_mt(SLOT + (I0 + i) * NSLOT);
                 };
-                fetch(0, 0);
+                auto item_nt = [](int i) {
+                    const int j = SLOT + (I0 + i) * NSLOT;
+                    return KL ? j - off_index(off_mt(j), 0) : j - low_index(low_mt(j), 0);
+                };
+                f32x4 acc[BN];
 #pragma unroll
-                for (int kp = 0; kp < NKP; ++kp) {
-                    const int cb = kp & 1;
-                    if (kp + 1 < NKP) fetch(kp + 1, cb ^ 1);
-                    __builtin_amdgcn_sched_barrier(0);
+                for (int i = 0; i < BN; ++i) acc[i] = zero4();
+                if constexpr (NK == 1) {
 #pragma unroll
-                    for (int i = 0; i < NMY; ++i) {
-                        acc[i] = mma32(fa[cb][0][i], fb[cb][0][i], acc[i]);
-                        if constexpr (F32IO) {
-                            acc[i] = mma32(fa[cb][0][i], fb[cb][FPL - 1][i], acc[i]);
-                            acc[i] = mma32(fa[cb][FPL - 1][i], fb[cb][0][i], acc[i]);
+                    for (int i = 0; i < BN; ++i) {
+                        const bf16* ar = Ab + (16 * item_mt(i) + c16) * SK + 4 * g;
+                        const bf16* br = Kb + (16 * item_nt(i) + c16) * SK + 4 * g;
+                        acc[i] = mma16(lds4(ar), lds4(br), acc[i]);
+                        if (F32IO) {
+                            acc[i] = mma16(lds4(ar), lds4(br + KPL), acc[i]);
+                            acc[i] = mma16(lds4(ar + KPL), lds4(br), acc[i]);
+                        }
+                    }
+                } else {
+                    // fragments of slice kp+1 are requested before the products of slice kp
+                    constexpr int NKP = NK / 2, FPL = F32IO ? 2 : 1;
+                    bf16x8 fa[2][FPL][BN], fb[2][FPL][BN];
+                    auto fetch = [&](int kp, int buf) {
+#pragma unroll
+                        for (int i = 0; i < BN; ++i) {
+                            const bf16* ar = Ab + (16 * item_mt(i) + c16) * SK + 32 * kp + 8 * g;
+                            const bf16* br = Kb + (16 * item_nt(i) + c16) * SK + 32 * kp + 8 * g;
+#pragma unroll
+                            for (int pl = 0; pl < FPL; ++pl) {
+                                fa[buf][pl][i] = lds8(ar + pl * KPL);
+                                fb[buf][pl][i] = lds8(br + pl * KPL);
+                            }
+                        }
+                    };
+                    fetch(0, 0);
+#pragma unroll
+                    for (int kp = 0; kp < NKP; ++kp) {
+                        const int cb = kp & 1;
+                        if (kp + 1 < NKP) fetch(kp + 1, cb ^ 1);
+                        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                        for (int i = 0; i < BN; ++i) {
+                            acc[i] = mma32(fa[cb][0][i], fb[cb][0][i], acc[i]);
+                            if constexpr (F32IO) {
+                                acc[i] = mma32(fa[cb][0][i], fb[cb][FPL - 1][i], acc[i]);
+                                acc[i] = mma32(fa[cb][FPL - 1][i], fb[cb][0][i], acc[i]);
+                            }
                         }
                     }
                 }
-            }
 #pragma unroll
-            for (int i = 0; i < NMY; ++i) {
-                const int mt = item_mt(i), nt = item_nt(i);
-                const int ic = 16 * nt + c16;
-                const float gci = gcp[ic];
-                const f32x4 gt = lds4f(gcp + 16 * mt + 4 * g);
-                f32x4 v;
-                if constexpr (KL) {
-                    const f32x4 bt = lds4f(G + CH + 16 * mt + 4 * g);
+                for (int i = 0; i < BN; ++i) {
+                    const int mt = item_mt(i), nt = item_nt(i);
+                    const int ic = 16 * nt + c16;
+                    const float gci = gcp[ic];
+                    const f32x4 gt = lds4f(gcp + 16 * mt + 4 * g);
+                    f32x4 v;
+                    if constexpr (KL) {
+                        const f32x4 bt = lds4f(G + CH + 16 * mt + 4 * g);
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) v[r] = -bt[r] * __expf(gt[r] - gci) * acc[i][r];
-                    store_tile_tr<SB, true>(sLT(b) + off_index(mt, nt) * BLK, NOFF * BLK, v, g, c16);
-                } else {
-                    const float cf = (FAM == FAM_GDN) ? p.scale : G[ic];  // SSD: dt of column i
+                        for (int r = 0; r < 4; ++r) v[r] = -bt[r] * __expf(gt[r] - gci) * acc[i][r];
+                        store_tile_tr<SB, true>(sLT(b) + off_index(mt, nt) * BLK, NOFF * BLK, v, g, c16);
+                    } else {
+                        const float cf = (FAM == FAM_GDN) ? p.scale : G[ic];  // SSD: dt of column i
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const float e = cf * __expf(gt[r] - gci) * acc[i][r];
-                        v[r] = (mt > nt || c16 <= 4 * g + r) ? e : 0.f;
+                        for (int r = 0; r < 4; ++r) {
+                            const float e = cf * __expf(gt[r] - gci) * acc[i][r];
+                            v[r] = (mt > nt || c16 <= 4 * g + r) ? e : 0.f;
+                        }
+                        store_tile_tr<SB, F32IO>(sPT(b) + low_index(mt, nt) * BLK, NPB * BLK, v, g, c16);
                     }
-                    store_tile_tr<SB, F32IO>(sPT(b) + low_index(mt, nt) * BLK, NPB * BLK, v, g, c16);
                 }
-            }
+            };
+            static_for<0, NBAT>(batch);
         }
     };
     using std::integral_constant;
