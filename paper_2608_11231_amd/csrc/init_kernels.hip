@@ -305,9 +305,9 @@ __global__ __launch_bounds__(64 * NW) void compose_gdn_kernel(ComposeArgs p) {
     // only takes S = B_{b0}), stages M_{j+1} and requests M_{j+2}.  Every step
     // has the same shape, so the state never comes straight from a load and
     // the prefetch registers carry the same in-flight loads at the top of
-    // every step.  Loads past the request's end re-read the block loaded
-    // just before (a cache hit; unconditional loads keep the prefetch
-    // registers single-valued).
+    // every step.  Loads past the request's end or its first invalid id
+    // re-read the last valid block (a cache hit; unconditional loads keep the
+    // prefetch registers single-valued).
     int32_t id0 = 0, id1 = 0, id2 = 0;  // ids at positions j, j + 1, j + 2
     if (b0 < b1) id0 = id_checked(b0);
     if (b0 + 1 < b1) id1 = id_checked(b0 + 1);
@@ -375,7 +375,7 @@ __global__ __launch_bounds__(64 * NW) void compose_gdn_kernel(ComposeArgs p) {
         // stage M_{j+1} (requested one step ago) and request M_{j+2}
         lds_barrier();  // every wave is done reading M_j (and the state halves)
         stage_m();
-        load_m(j + 2 < bad_at ? id2 : id1);
+        load_m(j + 2 < bad_at ? id2 : (j + 1 < bad_at ? id1 : id0));
 #pragma unroll
         for (int nt = 0; nt < NOWN; ++nt) S[nt] = acc[nt];
         if constexpr (CS) {
