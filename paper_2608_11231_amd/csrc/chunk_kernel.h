@@ -17,6 +17,9 @@
 // and for Mamba-2 (Eq. 2; q = C, k = B, v = x, gc = A_h * cumsum(dt)):
 //   O = diag(b) C S^T + lower(exp(gc_t - gc_i) * C B^T) diag(dt) X
 //   S <- b_C S + X^T diag(dt * w) B
+// Gated DeltaNet's state waves hold S / e^lam, lam being the log decay since
+// the last rescale: b_C then folds into lam, and b_t, w_t into per-token rows
+// that carry e^lam (see gate_rows).
 //
 // The work of a chunk splits into a state-independent part (gate prefix, the
 // token x token products and masks, inverses of the 16x16 diagonal blocks of
@@ -115,7 +118,9 @@ struct ChunkLds {
     static constexpr size_t K_SZ = al(size_t(PL) * CH * SK * 2);
     static constexpr size_t Q_SZ = HAS_Q ? al(size_t(PL) * CH * SK * 2) : 0;
     static constexpr size_t V_SZ = al(size_t(PL) * CH * SV * 2);
-    // gate rows: raw gate | beta | b | w | cumulative gate gc | b_C, gc_C (4) | beta b
+    // gate rows: raw gate | beta | b e^lam | w e^-lam' | cumulative gate gc |
+    // state factor, e^lam' (4) | beta b e^lam   (lam / lam': the stored state's
+    // log scale before / after the chunk; Mamba-2: lam = lam' = 0)
     static constexpr int BB_ROW = 5 * CH + 4;
     static constexpr size_t G_SZ = al((6 * CH + 4) * 4);
     static constexpr size_t LT_SZ = HAS_L ? al(size_t(NOFF) * BLK * 2 * 2) : 0;
@@ -681,7 +686,8 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                         }
                     }
                 }
-                // S <- b_C S + K^T diag(w) U   (all dk tiles and row tiles interleaved)
+                // S <- rho S + K^T diag(w) U   (rho: 1, or the rescale of gate_rows;
+                // all dk tiles and row tiles interleaved)
                 bf16x4 Wh[RT][NTC], Wl[RT][NTC];
                 if constexpr (NTC == 4) {
 #pragma unroll
@@ -824,7 +830,8 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
         // Per-chunk gate rows from this stager's own gate registers (run right
         // after commit, before the next prefetch reuses them): the in-chunk
         // cumulative log-gate in the wave's private row gcw (lane = token), and,
-        // from stager 0, the rows b = e^gc, w, gc, b_C, gc_C and beta b that the B-waves read.
+        // from stager 0, the rows b, w, gc, beta b and the state factors that the
+        // B-waves read.
         auto gate_rows = [&](int ci) {
             const int b = ci & 1;
             float* G = sG(b);
