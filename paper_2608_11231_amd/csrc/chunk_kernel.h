@@ -413,21 +413,25 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
             const int n = (int)((t1 - c0) < CH ? (t1 - c0) : CH);
             chunk_barrier();
             // ================= phase I: K S^T and the delta-rule right-hand side
+            // X: v of the chunk (state rows), later the substitution's right-hand
+            // side.  The scan and Mamba-2 read v here, ahead of K S^T; a Gated
+            // DeltaNet block summary reads it where it is combined (below), so its
+            // transition rows carry no value of X across the branch
+            constexpr bool V_EARLY = !SUMMARY || FAM == FAM_SSD;
             f32x4 X[RT][NTC];
             {
                 const bf16* Kb = sK(b);
                 const float* G = sG(b);
+                if (V_EARLY && load_v) {
 #pragma unroll
-                for (int rt = 0; rt < RT; ++rt)
+                    for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-                    for (int mt = 0; mt < NTC; ++mt) {
-                        X[rt][mt] = zero4();
-                        if (load_v) {
+                        for (int mt = 0; mt < NTC; ++mt) {
                             const int col = 16 * (RT * w + rt);
                             X[rt][mt] = to_f32(lds4_tr(sV(b), SV, 16 * mt, col, g, c16));
                             if (F32IO) X[rt][mt] += to_f32(lds4_tr(sV(b) + VPL, SV, 16 * mt, col, g, c16));
                         }
-                    }
+                }
                 if (FAM == FAM_GDN && with_out) {
                     // Gated DeltaNet: this chunk's output blocks P, shared by the B-waves
                     // (read after the barrier).  The stagers' second phase is full with
@@ -459,10 +463,16 @@ __global__ __launch_bounds__(64 * (NB + NA), (NB + NA) / 4) void chunk_kernel(Sc
                             const f32x4 bb = lds4f(G + Ly::BB_ROW + 16 * mt + 4 * g);
                             const f32x4 be = lds4f(G + CH + 16 * mt + 4 * g);
 #pragma unroll
-                            for (int rt = 0; rt < RT; ++rt)
+                            for (int rt = 0; rt < RT; ++rt) {
+                                if constexpr (!V_EARLY) {
+                                    const int col = 16 * (RT * w + rt);
+                                    X[rt][mt] = to_f32(lds4_tr(sV(b), SV, 16 * mt, col, g, c16));
+                                    if (F32IO) X[rt][mt] += to_f32(lds4_tr(sV(b) + VPL, SV, 16 * mt, col, g, c16));
+                                }
 #pragma unroll
                                 for (int r = 0; r < 4; ++r)
                                     X[rt][mt][r] = be[r] * X[rt][mt][r] - bb[r] * ks[rt][mt][r];
+                            }
                         }
                     } else {
 #pragma unroll
