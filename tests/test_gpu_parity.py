@@ -482,3 +482,27 @@ def test_fold_view_keeps_blocks_reused_later():
     assert rel_slices(got_M[[0, 1, 2, 4]], M[[0, 1, 2, 4]]) < STATE_TOL
     assert np.array_equal(got_M[3], np.broadcast_to(np.eye(64, dtype=np.float32), got_M[3].shape))
     assert rel_slices(_np(G.S_exact), R.init_compose(w, B, M)) < STATE_TOL
+
+
+@pytest.mark.parametrize("x_mu", [-3.0, 0.0], ids=["rescale-every-few-chunks", "rescale-every-chunk"])
+def test_gdn_state_rescale(x_mu):
+    """The state waves hold S / e^lam and rescale once lam would drop below
+    -32 (the chunk decays of Eq. 3 moved into the gate rows).  With log-decays
+    of about -5 per 64-token chunk the rescale comes about every seventh chunk
+    (once in each 12-chunk block, twice in the 15-chunk online stream) and the
+    blocks' transitions stay near e^-60, inside fp32's range; with about -50
+    per chunk it comes in every chunk.  Summaries and the scan are checked
+    against the oracle; at -50 per chunk a block's transition (about e^-600)
+    is below fp32's range, so only its state, the outputs and the final state
+    are compared."""
+    layer = I.Layer(I.GDN, 1, 2, 128, 128, 64, "bf16", "bf16")
+    w = I.build_workload(f"rescale{x_mu}", layer, [[768, 700]], [900], I.GateLaw(x_mu=x_mu, beta_mu=0.0), 31,
+                         scale=0.75)
+    G = gpu_io.GpuWorkload(w)
+    G.block_summary()
+    torch.cuda.synchronize()
+    B, M = R.summaries(w)
+    assert rel_slices(_np(G.B_pool), B) < STATE_TOL
+    if x_mu < -1.0:
+        assert rel_slices(_np(G.M_pool), M) < STATE_TOL
+    _scan_check(w, G, R.init_compose(w, B, M))
